@@ -1,0 +1,163 @@
+"""Benchmark of the dilated-attention forward pass on one MI355X.
+
+One step = one dilated_attn_fwd call (attention stage + combine stage) over
+the N=32768, H=12, D=64 bf16 workload with the five patterns
+(2048,1) (4096,2) (8192,4) (16384,6) (32768,12), inputs resident in HBM.
+
+Prints one JSON line: effective TFLOP/s over the exact sparse flops (4*D per
+unmasked query-key pair), tokens/s, per-stage times measured with HIP events
+recorded by the library on the call's stream, the attention stage's MFMA
+roofline fraction, and the CPU oracle timed on a bounded sample on this host.
+"""
+from __future__ import annotations
+
+import argparse
+import json
+import os
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+METRIC = "dilated-attn fwd effective TFLOP/s + tokens/s at N=32K, MFMA util %"
+DEFAULT_WORKLOAD = "n32k_h12_d64_5pat"
+PEAK_BF16_TFLOPS = 2500.0     # MI355X dense bf16 MFMA
+PEAK_F32_TFLOPS = 157.3       # MI355X fp32 vector
+PEAK_HBM_GBS = 8000.0         # MI355X HBM3E
+PROFILED_TRAFFIC = os.path.join(ROOT, "profiles", "traffic.json")
+
+
+def parse():
+    ap = argparse.ArgumentParser(description=__doc__)
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=50)
+    ap.add_argument("--warmup", type=int, default=5)
+    ap.add_argument("--workload", default=DEFAULT_WORKLOAD)
+    ap.add_argument("--cpu-seconds", type=float, default=12.0,
+                    help="minimum CPU time spent on the oracle sample (0 skips the CPU baseline)")
+    return ap.parse_args()
+
+
+def cpu_baseline(wl, q, k, v, min_seconds):
+    """Time the CPU oracle, as it stands, on whole heads of the same workload
+    until at least `min_seconds` have passed; report flops/s over those heads."""
+    import numpy as np
+
+    import oracle
+    try:
+        from threadpoolctl import threadpool_info
+        pools = threadpool_info()
+        threads = max((p.get("num_threads", 1) for p in pools), default=1)
+        blas = ",".join(sorted({p.get("internal_api", "?") for p in pools}))
+    except Exception:  # threadpoolctl missing or failing: report the affinity count
+        threads, blas = len(os.sched_getaffinity(0)), "unknown"
+    q64 = q.to("cpu").double().numpy()
+    k64 = k.to("cpu").double().numpy()
+    v64 = v.to("cpu").double().numpy()
+    pats = list(wl.patterns)
+    done, flops = [], 0
+    t0 = time.perf_counter()
+    for h in range(wl.H):
+        oracle.dilated_attention_ref(q64, k64, v64, pats, wl.causal, heads=[h])
+        done.append(h)
+        flops += 4 * wl.D * wl.B * sum(
+            (L * (L + 1) // 2 if wl.causal else L * L)
+            for (w, r) in pats for g in range(oracle.num_segments(wl.N, w))
+            for L in [oracle.index_set(wl.N, w, r, h, g).size])
+        if time.perf_counter() - t0 >= min_seconds:
+            break
+    dt = time.perf_counter() - t0
+    return {
+        "value": flops / dt / 1e12, "unit": "TFLOP/s", "cores": int(threads), "kind": "oracle",
+        "sample": f"{len(done)} of {wl.H} heads of {wl.name} (all patterns, all rows), fp64 NumPy "
+                  f"({blas}), {dt:.1f} s",
+        "tokens_per_s": wl.B * wl.N * len(done) / wl.H / dt,
+        "host_cpus": len(os.sched_getaffinity(0)),
+    }
+
+
+def main():
+    args = parse()
+    if args.gpus != 1:
+        print(f"bench.py: this build runs on one GPU only (asked for --gpus {args.gpus}); "
+              "the sequence-parallel multi-GPU path is not built", file=sys.stderr)
+        sys.exit(2)
+    import torch
+
+    import workloads
+    from paper_2307_02486_amd import StageTimer, dilated_attn, plan, workspace_for
+
+    if not torch.cuda.is_available():
+        print("bench.py: no HIP device visible", file=sys.stderr)
+        sys.exit(1)
+    wl = workloads.BY_NAME[args.workload]
+    dev = torch.device("cuda:0")
+    torch.cuda.set_device(dev)
+    q, k, v = workloads.make_qkv(wl, device=dev)
+    pats = list(wl.patterns)
+    info = plan(wl.B, wl.N, wl.H, wl.D, pats, wl.causal, wl.torch_dtype)
+    out = torch.empty_like(q)
+    lse = torch.empty((wl.B, wl.H, wl.N), dtype=torch.float32, device=dev)
+    ws = workspace_for(q, pats, wl.causal)
+    stream = torch.cuda.current_stream(dev)
+
+    def step():
+        dilated_attn(q, k, v, pats, wl.causal, out=out, lse=lse, workspace=ws, stream=stream)
+
+    for _ in range(args.warmup):
+        step()
+    torch.cuda.synchronize()
+    t_start = torch.cuda.Event(enable_timing=True)
+    t_end = torch.cuda.Event(enable_timing=True)
+    with StageTimer(capacity=max(1, args.steps)) as st:
+        torch.cuda.synchronize()
+        t_start.record(stream)
+        for _ in range(args.steps):
+            step()
+        t_end.record(stream)
+        torch.cuda.synchronize()
+    total_ms = t_start.elapsed_time(t_end)
+    ms = total_ms / args.steps
+    ms_attn = st.ms_attention / max(1, st.calls)
+    ms_comb = st.ms_combine / max(1, st.calls)
+    flops = info["sparse_flops"]
+    tflops = flops / (ms * 1e-3) / 1e12
+    attn_tflops = flops / (ms_attn * 1e-3) / 1e12
+    comb_gbs = info["bytes_combine"] / (ms_comb * 1e-3) / 1e9
+    peak = PEAK_BF16_TFLOPS if wl.dtype == "bf16" else PEAK_F32_TFLOPS
+    traffic = None
+    if os.path.exists(PROFILED_TRAFFIC):
+        with open(PROFILED_TRAFFIC) as f:
+            traffic = json.load(f).get(wl.name, {}).get("attention_bytes_per_launch")
+    res = {
+        "metric": METRIC,
+        "value": round(tflops, 3),
+        "unit": "TFLOP/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": round(ms, 5),
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": wl.dtype,
+        "data": "synthetic (seeded N(0, sigma^2), rounded to dtype)",
+        "config": wl.describe(),
+        "tokens_per_s": round(wl.B * wl.N / (ms * 1e-3), 1),
+        "sparse_flops": flops,
+        "attention_stage": {"ms": round(ms_attn, 5), "tflops": round(attn_tflops, 3),
+                            "frac_of_mfma_peak": round(attn_tflops / peak, 4)},
+        "combine_stage": {"ms": round(ms_comb, 5), "algorithmic_bytes": info["bytes_combine"],
+                          "gbps": round(comb_gbs, 1), "frac_of_hbm_peak": round(comb_gbs / PEAK_HBM_GBS, 4)},
+        "roofline": {"bound": "mfma", "achieved": round(attn_tflops, 3), "peak": peak,
+                     "unit": "TFLOP/s", "frac": round(attn_tflops / peak, 4), "traffic": traffic},
+        "cpu_baseline": None,
+    }
+    if args.cpu_seconds > 0:
+        res["cpu_baseline"] = cpu_baseline(wl, q, k, v, args.cpu_seconds)
+    print(json.dumps(res), flush=True)
+
+
+if __name__ == "__main__":
+    main()

@@ -1,0 +1,141 @@
+/*
+ * dilated_attn.h - C ABI of the MI355X (gfx950) dilated-attention forward pass.
+ *
+ * The operator is LongNet's dilated attention (Sec. 2.2-2.3 of the paper):
+ *   1. split the sequence into segments of length w_i          (Sec. 2.2, Eqs. 3-5)
+ *   2. in each segment keep every r_i-th row, starting at the  (Sec. 2.3, s_j = j mod r)
+ *      head's offset h mod r_i
+ *   3. dense softmax attention inside each sparsified segment  (Sec. 2.2, Eq. 6)
+ *   4. scatter the rows back and mix the k patterns, each      (Sec. 2.2, Eqs. 7-10)
+ *      weighted by its softmax denominator
+ *
+ * Semantics fixed by this library where the paper is silent:
+ *   - scores are scaled by softmax_scale (0 selects 1/sqrt(D));
+ *   - causal != 0: inside a sparsified segment, a query sees the kept rows at
+ *     or before its own position; causal == 0: it sees every kept row;
+ *   - the offset is segment-local: segment g keeps rows p in
+ *     [g*w, min((g+1)*w, N)) with (p - g*w) mod r == h mod r, heads from 0;
+ *     a last segment shorter than w is truncated, w > N means one segment;
+ *   - a pattern's weight is its unshifted softmax denominator; a pattern that
+ *     does not keep a row contributes nothing there; duplicate patterns count
+ *     twice; a row kept by no pattern gets out = 0 and lse = -inf.
+ *
+ * Layouts (row-major, contiguous, no strides):
+ *   q, k, v, out : [B, N, H, D] elements of `dtype`
+ *   lse          : [B, H, N] float32, natural log of the summed denominators
+ *
+ * Every integer is 64-bit on the ABI.  Limits: 1 <= B, 1 <= N, N + H < 2^31,
+ * 1 <= H < 2^16, D in {32, 64, 128}, 1 <= num_patterns <= DA_MAX_PATTERNS,
+ * 1 <= r_i <= w_i.
+ */
+#ifndef DILATED_ATTN_H
+#define DILATED_ATTN_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+#define DA_MAX_PATTERNS 16
+
+/* One dilated pattern (Sec. 2.2, the pairs {r_i, w_i}). */
+typedef struct {
+  int64_t w; /* segment length, >= 1 */
+  int64_t r; /* dilation rate, 1 <= r <= w */
+} da_pattern_t;
+
+/* Element types of q, k, v and out. */
+enum { DA_F32 = 0, DA_BF16 = 1 };
+
+/* Error codes.  Every entry point returns DA_OK or one of these; on error
+ * nothing is written to any caller buffer and nothing is launched. */
+enum {
+  DA_OK = 0,
+  DA_EINVAL = -1,       /* null pointer, non-positive size, bad pattern list,
+                           out aliasing an input, size beyond the limits  */
+  DA_EUNSUPPORTED = -2, /* head dim or dtype this build has no kernel for */
+  DA_EWORKSPACE = -3,   /* workspace smaller than dilated_attn_plan asks  */
+  DA_EALIGN = -4,       /* a device pointer not 16-byte aligned           */
+  DA_EHIP = -5          /* the HIP runtime reported an error at launch    */
+};
+
+/* Sizes and work of one call, filled by dilated_attn_plan. */
+typedef struct {
+  uint64_t workspace_bytes; /* device memory the caller passes to fwd        */
+  int64_t num_work_items;   /* attention work items (pattern, b, h, segment,
+                               query tile) launched by fwd                    */
+  int64_t covered_rows;     /* sum over patterns of kept (b, row, head) rows  */
+  double sparse_flops;      /* 4*D per unmasked (query, key) pair, the work of
+                               Sec. 2.4 counted exactly                       */
+  double bytes_attn;        /* algorithmic HBM bytes of the attention stage:
+                               kept q/k/v rows read once, per-pattern output
+                               and lse written once                          */
+  double bytes_combine;     /* algorithmic HBM bytes of the combine stage:
+                               per-pattern output and lse read once, out and
+                               lse written once                               */
+} da_plan_info_t;
+
+/*
+ * dilated_attn_plan - validate a problem and report its workspace and work.
+ *
+ * Host only: touches no device and may be called without a GPU.  Arguments
+ * are those of dilated_attn_fwd without the buffers.  `patterns` points to
+ * num_patterns host structs, read during the call only.  Returns DA_OK and
+ * fills *info, or a negative error code (info untouched).
+ */
+int dilated_attn_plan(int64_t B, int64_t N, int64_t H, int64_t D,
+                      const da_pattern_t* patterns, int64_t num_patterns,
+                      int64_t causal, int64_t dtype, float softmax_scale,
+                      da_plan_info_t* info);
+
+/*
+ * dilated_attn_fwd - dilated-attention forward pass (Sec. 2.2-2.3).
+ *
+ * q, k, v   device pointers, [B, N, H, D] of dtype, read only.
+ * out       device pointer, [B, N, H, D] of dtype, written (every element).
+ * lse       device pointer, [B, H, N] float32, written (every element).
+ * patterns  host pointer to num_patterns (w, r) pairs, read during the call.
+ * workspace device scratch of at least info.workspace_bytes from
+ *           dilated_attn_plan, owned by the caller; contents on entry are
+ *           ignored and on return are unspecified.
+ * stream    a hipStream_t (NULL = the default stream).  Work is enqueued
+ *           asynchronously; buffers must stay valid until the stream reaches
+ *           this point.  Nothing is allocated and nothing synchronises.
+ *
+ * All device pointers must be 16-byte aligned and out must not overlap q, k
+ * or v.  Returns DA_OK or a negative error code; before any launch, every
+ * argument is checked and an error leaves all buffers untouched.
+ */
+int dilated_attn_fwd(const void* q, const void* k, const void* v, void* out,
+                     float* lse, int64_t B, int64_t N, int64_t H, int64_t D,
+                     const da_pattern_t* patterns, int64_t num_patterns,
+                     int64_t causal, int64_t dtype, float softmax_scale,
+                     void* workspace, uint64_t workspace_bytes, void* stream);
+
+/* Human-readable text for an error code (static storage, never NULL). */
+const char* dilated_attn_strerror(int code);
+
+/*
+ * Stage timing, a profiling aid (not part of the operator).
+ *
+ * dilated_attn_profile_begin(capacity) creates 3*capacity HIP events on the
+ * current device; each of the next `capacity` dilated_attn_fwd calls records
+ * one event before the attention stage, one between the stages and one after
+ * the combine stage, on the call's stream (calls beyond capacity are not
+ * timed).  dilated_attn_profile_end waits for the recorded events, writes the
+ * summed durations of the two stages in milliseconds and the number of timed
+ * calls, and destroys the events.  capacity must be in [1, 1<<20]; any
+ * pointer argument of profile_end may be NULL.  Not thread safe: one profiling
+ * window per process at a time (DA_EINVAL otherwise); DA_EHIP if an event
+ * call fails.
+ */
+int dilated_attn_profile_begin(int64_t capacity);
+int dilated_attn_profile_end(double* ms_attention, double* ms_combine, int64_t* calls);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* DILATED_ATTN_H */

@@ -1,0 +1,70 @@
+"""Build libdilated_attn.so (HIP for gfx950) in-tree with hipcc.
+
+Usage: python -m paper_2307_02486_amd.build   (or call build()).
+Always recompiles; the library lands next to this file.
+"""
+from __future__ import annotations
+
+import os
+import shutil
+import subprocess
+import sys
+import tempfile
+
+HERE = os.path.dirname(os.path.abspath(__file__))
+CSRC = os.path.join(HERE, "csrc")
+ROOT = os.path.dirname(HERE)
+INCLUDE = os.path.join(ROOT, "include")
+LIB_NAME = "libdilated_attn.so"
+LIB_PATH = os.path.join(HERE, LIB_NAME)
+
+HIP_SOURCES = ["attn_fwd.hip", "combine.hip"]
+HOST_SOURCES = ["plan.cpp", "api.cpp"]
+
+ARCH = "gfx950"
+COMMON = ["-O3", "-std=c++17", "-fPIC", "-Wall", "-I", INCLUDE, "-I", CSRC]
+# Packed fp32 instructions stay off (the compiler must not form v_pk_* f32 ops).
+DEVICE_FLAGS = [f"--offload-arch={ARCH}", "-Xclang", "-target-feature", "-Xclang", "-packed-fp32-ops"]
+
+
+def _hipcc() -> str:
+    for cand in (shutil.which("hipcc"), "/opt/rocm/bin/hipcc"):
+        if cand and os.path.exists(cand):
+            return cand
+    raise RuntimeError("hipcc not found: the HIP library cannot be built")
+
+
+def _run(cmd, verbose):
+    if verbose:
+        print(" ".join(cmd), flush=True)
+    res = subprocess.run(cmd, capture_output=True, text=True)
+    if res.returncode != 0:
+        sys.stderr.write(res.stdout + res.stderr)
+        raise RuntimeError(f"build step failed: {' '.join(cmd)}")
+    # keep real warnings visible, drop the host pass's note about the packed-fp32 feature
+    msgs = [l for l in (res.stderr or "").splitlines() if "packed-fp32-ops" not in l and l.strip()]
+    if msgs and verbose:
+        sys.stderr.write("\n".join(msgs) + "\n")
+
+
+def build(verbose: bool = True) -> str:
+    hipcc = _hipcc()
+    with tempfile.TemporaryDirectory(prefix="dilattn_build_") as tmp:
+        objs = []
+        for src in HIP_SOURCES:
+            obj = os.path.join(tmp, src + ".o")
+            _run([hipcc, *COMMON, *DEVICE_FLAGS, "-x", "hip", "-c", os.path.join(CSRC, src), "-o", obj], verbose)
+            objs.append(obj)
+        for src in HOST_SOURCES:
+            obj = os.path.join(tmp, src + ".o")
+            _run([hipcc, *COMMON, "-c", os.path.join(CSRC, src), "-o", obj], verbose)
+            objs.append(obj)
+        tmp_lib = os.path.join(tmp, LIB_NAME)
+        _run([hipcc, *DEVICE_FLAGS, "-shared", "-fPIC", *objs, "-o", tmp_lib], verbose)
+        shutil.move(tmp_lib, LIB_PATH + ".tmp")
+        os.replace(LIB_PATH + ".tmp", LIB_PATH)
+    return LIB_PATH
+
+
+if __name__ == "__main__":
+    print(build())

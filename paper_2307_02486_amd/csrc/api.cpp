@@ -1,0 +1,143 @@
+// C ABI of the dilated-attention forward pass (declared in include/dilated_attn.h).
+#include <hip/hip_runtime.h>
+
+#include <cstdint>
+#include <vector>
+
+#include "kernels.h"
+#include "plan.h"
+
+namespace {
+
+bool overlaps(const void* a, uint64_t na, const void* b, uint64_t nb) {
+  const uintptr_t x = reinterpret_cast<uintptr_t>(a);
+  const uintptr_t y = reinterpret_cast<uintptr_t>(b);
+  return x < y + nb && y < x + na;
+}
+
+bool aligned16(const void* p) { return (reinterpret_cast<uintptr_t>(p) & 15u) == 0; }
+
+// Profiling window of dilated_attn_profile_begin/end: three events per call.
+struct ProfileWindow {
+  bool active = false;
+  int64_t capacity = 0;
+  int64_t used = 0;
+  std::vector<hipEvent_t> ev;  // [call][0..2]
+};
+ProfileWindow g_prof;
+
+void destroy_events(ProfileWindow& w) {
+  for (hipEvent_t e : w.ev)
+    if (e) (void)hipEventDestroy(e);
+  w.ev.clear();
+  w.active = false;
+  w.capacity = w.used = 0;
+}
+
+}  // namespace
+
+extern "C" {
+
+int dilated_attn_plan(int64_t B, int64_t N, int64_t H, int64_t D, const da_pattern_t* patterns,
+                      int64_t num_patterns, int64_t causal, int64_t dtype, float softmax_scale,
+                      da_plan_info_t* info) {
+  if (!info) return DA_EINVAL;
+  da::Plan p;
+  const int rc = da::make_plan(B, N, H, D, patterns, num_patterns, causal, dtype, softmax_scale, &p);
+  if (rc != DA_OK) return rc;
+  info->workspace_bytes = p.workspace_bytes;
+  info->num_work_items = p.total_items;
+  info->covered_rows = p.covered_rows;
+  info->sparse_flops = p.sparse_flops;
+  info->bytes_attn = p.bytes_attn;
+  info->bytes_combine = p.bytes_combine;
+  return DA_OK;
+}
+
+int dilated_attn_fwd(const void* q, const void* k, const void* v, void* out, float* lse,
+                     int64_t B, int64_t N, int64_t H, int64_t D, const da_pattern_t* patterns,
+                     int64_t num_patterns, int64_t causal, int64_t dtype, float softmax_scale,
+                     void* workspace, uint64_t workspace_bytes, void* stream) {
+  da::Plan p;
+  const int rc = da::make_plan(B, N, H, D, patterns, num_patterns, causal, dtype, softmax_scale, &p);
+  if (rc != DA_OK) return rc;
+  if (!q || !k || !v || !out || !lse || !workspace) return DA_EINVAL;
+  if (!aligned16(q) || !aligned16(k) || !aligned16(v) || !aligned16(out) || !aligned16(lse) ||
+      !aligned16(workspace))
+    return DA_EALIGN;
+  const uint64_t esize = dtype == DA_BF16 ? 2 : 4;
+  const uint64_t tensor_bytes = static_cast<uint64_t>(B * N * H * D) * esize;
+  const uint64_t lse_bytes = static_cast<uint64_t>(B * H * N) * 4;
+  if (overlaps(out, tensor_bytes, q, tensor_bytes) || overlaps(out, tensor_bytes, k, tensor_bytes) ||
+      overlaps(out, tensor_bytes, v, tensor_bytes) || overlaps(lse, lse_bytes, out, tensor_bytes) ||
+      overlaps(lse, lse_bytes, q, tensor_bytes) || overlaps(lse, lse_bytes, k, tensor_bytes) ||
+      overlaps(lse, lse_bytes, v, tensor_bytes))
+    return DA_EINVAL;
+  if (workspace_bytes < p.workspace_bytes) return DA_EWORKSPACE;
+  const void* bufs[5] = {q, k, v, out, lse};
+  const uint64_t sizes[5] = {tensor_bytes, tensor_bytes, tensor_bytes, tensor_bytes, lse_bytes};
+  for (int i = 0; i < 5; ++i)
+    if (overlaps(workspace, p.workspace_bytes, bufs[i], sizes[i])) return DA_EINVAL;
+
+  hipStream_t s = static_cast<hipStream_t>(stream);
+  hipEvent_t* ev = nullptr;
+  if (g_prof.active && g_prof.used < g_prof.capacity) ev = &g_prof.ev[3 * g_prof.used++];
+  if (ev && hipEventRecord(ev[0], s) != hipSuccess) return DA_EHIP;
+  if (da::launch_attention(p, q, k, v, workspace, s) != hipSuccess) return DA_EHIP;
+  if (ev && hipEventRecord(ev[1], s) != hipSuccess) return DA_EHIP;
+  if (da::launch_combine(p, workspace, out, lse, s) != hipSuccess) return DA_EHIP;
+  if (ev && hipEventRecord(ev[2], s) != hipSuccess) return DA_EHIP;
+  return DA_OK;
+}
+
+int dilated_attn_profile_begin(int64_t capacity) {
+  if (g_prof.active || capacity < 1 || capacity > (int64_t{1} << 20)) return DA_EINVAL;
+  g_prof.ev.assign(static_cast<size_t>(3 * capacity), nullptr);
+  for (hipEvent_t& e : g_prof.ev) {
+    if (hipEventCreate(&e) != hipSuccess) {
+      e = nullptr;
+      destroy_events(g_prof);
+      return DA_EHIP;
+    }
+  }
+  g_prof.capacity = capacity;
+  g_prof.used = 0;
+  g_prof.active = true;
+  return DA_OK;
+}
+
+int dilated_attn_profile_end(double* ms_attention, double* ms_combine, int64_t* calls) {
+  if (!g_prof.active) return DA_EINVAL;
+  double ta = 0.0, tc = 0.0;
+  int rc = DA_OK;
+  if (g_prof.used > 0 && hipEventSynchronize(g_prof.ev[3 * g_prof.used - 1]) != hipSuccess) rc = DA_EHIP;
+  for (int64_t i = 0; i < g_prof.used && rc == DA_OK; ++i) {
+    float a = 0.0f, c = 0.0f;
+    if (hipEventElapsedTime(&a, g_prof.ev[3 * i], g_prof.ev[3 * i + 1]) != hipSuccess ||
+        hipEventElapsedTime(&c, g_prof.ev[3 * i + 1], g_prof.ev[3 * i + 2]) != hipSuccess)
+      rc = DA_EHIP;
+    ta += a;
+    tc += c;
+  }
+  const int64_t n = g_prof.used;
+  destroy_events(g_prof);
+  if (rc != DA_OK) return rc;
+  if (ms_attention) *ms_attention = ta;
+  if (ms_combine) *ms_combine = tc;
+  if (calls) *calls = n;
+  return DA_OK;
+}
+
+const char* dilated_attn_strerror(int code) {
+  switch (code) {
+    case DA_OK: return "success";
+    case DA_EINVAL: return "invalid argument (null pointer, size, pattern list or overlapping buffers)";
+    case DA_EUNSUPPORTED: return "unsupported head dimension or dtype";
+    case DA_EWORKSPACE: return "workspace smaller than dilated_attn_plan requires";
+    case DA_EALIGN: return "device pointer not 16-byte aligned";
+    case DA_EHIP: return "HIP runtime error at kernel launch";
+    default: return "unknown error code";
+  }
+}
+
+}  // extern "C"

@@ -1,0 +1,423 @@
+// Stage 1 of the dilated-attention forward pass on gfx950: per pattern, per
+// (batch, head, segment), gather the kept rows (every r-th row from the head's
+// offset, Sec. 2.2 Eqs. 3-5 and Sec. 2.3) straight from HBM into registers and
+// LDS, and run softmax attention on them (Sec. 2.2 Eq. 6) with an online
+// softmax.  The normalised output rows and their log-sum-exp go to the
+// workspace in compact per-pattern order [b][h][segment][t][D].
+//
+// bf16 path: one work item = 128 query rows of one sparsified segment, four
+// waves of 32 rows.  Scores are computed transposed, S^T = K Q^T, with
+// v_mfma_f32_32x32x16_bf16, so that every lane owns one query row: the row
+// max needs one exchange between the two half-waves and the probabilities can
+// feed the P V product (computed as O^T = V^T P^T) straight from registers.
+// V is stored transposed in LDS, with keys permuted inside each group of 16
+// so a lane's eight keys of one MFMA step are contiguous.
+//
+// f32 path: a plain VALU kernel (one thread per query row) used for float32
+// inputs, where accuracy rather than speed is the point.
+#include <hip/hip_runtime.h>
+
+#include "kernels.h"
+
+namespace da {
+namespace {
+
+typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
+typedef float f32x16 __attribute__((ext_vector_type(16)));
+typedef float f32x4 __attribute__((ext_vector_type(4)));
+typedef unsigned int u32x4 __attribute__((ext_vector_type(4)));
+typedef unsigned short u16;
+
+constexpr float kLn2 = 0.693147180559945309f;
+constexpr float kLog2e = 1.442695040888963407f;
+constexpr float kNegBig = -1.0e30f;   // finite "minus infinity" for running maxima
+
+struct PatArgs {
+  int32_t w, r, nseg, lmax, ntiles, item_begin;
+  int64_t o_off;    // float offset of this pattern's output rows in the workspace
+  int64_t lse_off;  // float offset of this pattern's lse in the workspace
+};
+
+struct AttnArgs {
+  const void* q;
+  const void* k;
+  const void* v;
+  float* ws;
+  int32_t B, N, H, npat, causal, total_items;
+  float scale_log2;  // softmax scale times log2(e): scores go to exp2 directly
+  PatArgs pat[DA_MAX_PATTERNS];
+};
+
+// One attention work item: which segment of which pattern, and which query tile.
+struct Item {
+  int pi;          // pattern index
+  int b, h, g;     // batch, head, segment
+  int unit;        // (b*H + h)*nseg + g
+  int tq;          // query tile index inside the segment
+  int L;           // kept rows of this (head, segment)
+  int64_t row0;    // [B,N,H] row index of kept row t = 0
+  int64_t rstride; // row-index step between consecutive kept rows (r*H)
+};
+
+// Work items are ordered pattern by pattern; inside a pattern, unit by unit
+// (segment fastest), and inside a unit the query tiles run from the last (the
+// longest under a causal mask) to the first.
+__device__ inline bool decode_item(const AttnArgs& a, int item, int block_m, Item& it) {
+  int pi = 0;
+  while (pi + 1 < a.npat && item >= a.pat[pi + 1].item_begin) ++pi;
+  const PatArgs& P = a.pat[pi];
+  const int rem = item - P.item_begin;
+  const int unit = rem / P.ntiles;
+  it.tq = P.ntiles - 1 - (rem - unit * P.ntiles);
+  it.pi = pi;
+  it.unit = unit;
+  it.g = unit % P.nseg;
+  const int bh = unit / P.nseg;
+  it.h = bh % a.H;
+  it.b = bh / a.H;
+  const int s = it.h % P.r;
+  const int seg_start = it.g * P.w;
+  const int seg_len = min(P.w, a.N - seg_start);
+  it.L = seg_len > s ? (seg_len - s + P.r - 1) / P.r : 0;
+  it.row0 = ((int64_t)it.b * a.N + seg_start + s) * a.H + it.h;
+  it.rstride = (int64_t)P.r * a.H;
+  return it.tq * block_m < it.L;
+}
+
+// ---------------------------------------------------------------------------
+// bf16 MFMA kernel
+// ---------------------------------------------------------------------------
+constexpr int kBM = 128;      // query rows per work item
+constexpr int kBN = 64;       // keys per K/V tile
+constexpr int kThreads = 256; // four waves
+
+// Position of key `key` (0..kBN-1) inside a transposed V row: within each group
+// of 16 keys, keys {0-3, 8-11} come first and {4-7, 12-15} second, which is the
+// order in which the upper and lower half-waves hold them after S^T.
+__device__ inline int vt_pos(int key) {
+  const int k16 = key & 15;
+  return (key & ~15) | (((k16 >> 2) & 1) << 3) | ((k16 >> 3) << 2) | (k16 & 3);
+}
+
+template <int D>
+struct SmemBf16 {
+  static constexpr int KSTR = D + 8;    // row pitch (elements) of the K tile
+  static constexpr int VSTR = kBN + 8;  // row pitch (elements) of the V^T tile
+  u16 k[kBN * KSTR];
+  u16 vt[D * VSTR];
+};
+
+__device__ inline u32x4 load16(const u16* p) { return *reinterpret_cast<const u32x4*>(p); }
+
+template <int D>
+__global__ __launch_bounds__(kThreads) void attn_fwd_bf16(AttnArgs a) {
+  static_assert(D % 32 == 0, "head dim must be a multiple of 32");
+  constexpr int KC = D / 16;  // MFMA k-steps over the head dim
+  constexpr int DB = D / 32;  // 32-wide blocks of the head dim in O^T
+  __shared__ __attribute__((aligned(16))) SmemBf16<D> sm;
+
+  Item it;
+  if (!decode_item(a, blockIdx.x, kBM, it)) return;
+  const PatArgs& P = a.pat[it.pi];
+  const u16* __restrict__ qg = static_cast<const u16*>(a.q);
+  const u16* __restrict__ kg = static_cast<const u16*>(a.k);
+  const u16* __restrict__ vg = static_cast<const u16*>(a.v);
+
+  const int tid = threadIdx.x;
+  const int lane = tid & 63;
+  const int wv = tid >> 6;
+  const int qr = lane & 31;   // query column of this lane in S^T / O^T
+  const int hi = lane >> 5;   // half-wave
+  const int L = it.L;
+  const int q0 = it.tq * kBM;
+  const int qend = min(q0 + kBM, L);
+  const int tq_row = q0 + wv * 32 + qr;  // this lane's query (kept-row index)
+  const bool q_valid = tq_row < L;
+
+  // Q^T operand: lane holds query tq_row, head-dim slice [16c + 8hi, +8).
+  bf16x8 qreg[KC];
+  {
+    const u16* qp = qg + (it.row0 + (int64_t)tq_row * it.rstride) * D + 8 * hi;
+#pragma unroll
+    for (int c = 0; c < KC; ++c) {
+      u32x4 x = q_valid ? load16(qp + 16 * c) : u32x4{0, 0, 0, 0};
+      qreg[c] = __builtin_bit_cast(bf16x8, x);
+    }
+  }
+
+  f32x16 acc_o[DB];
+#pragma unroll
+  for (int db = 0; db < DB; ++db) acc_o[db] = f32x16{};
+  float m_run = kNegBig;  // running max of scaled scores (log2 domain)
+  float l_run = 0.0f;     // this half-wave's share of the running denominator
+
+  const int kv_end = a.causal ? qend : L;
+  const int ntile = (kv_end + kBN - 1) / kBN;
+  const int wq_lo = q0 + wv * 32;  // smallest query of this wave
+
+  for (int jt = 0; jt < ntile; ++jt) {
+    const int k0 = jt * kBN;
+    __syncthreads();
+    // K tile: row-major [key][d], 16-byte chunks, 8 lanes per 128-byte row.
+#pragma unroll
+    for (int task = tid; task < kBN * D / 8; task += kThreads) {
+      const int key = task / (D / 8);
+      const int dc = task % (D / 8);
+      const int t = k0 + key;
+      u32x4 x = u32x4{0, 0, 0, 0};
+      if (t < L) x = load16(kg + (it.row0 + (int64_t)t * it.rstride) * D + dc * 8);
+      *reinterpret_cast<u32x4*>(&sm.k[key * SmemBf16<D>::KSTR + dc * 8]) = x;
+    }
+    // V tile transposed: a thread takes keys (2kp, 2kp+1) of one 8-wide chunk
+    // of the head dim and writes 8 key pairs as 32-bit words.
+#pragma unroll
+    for (int task = tid; task < (kBN / 2) * (D / 8); task += kThreads) {
+      const int kp = task & 31;
+      const int dc = task >> 5;
+      const int t = k0 + 2 * kp;
+      u32x4 x0 = u32x4{0, 0, 0, 0}, x1 = u32x4{0, 0, 0, 0};
+      const u16* vp = vg + (it.row0 + (int64_t)t * it.rstride) * D + dc * 8;
+      if (t < L) x0 = load16(vp);
+      if (t + 1 < L) x1 = load16(vp + it.rstride * D);
+      const int pos = vt_pos(2 * kp);
+#pragma unroll
+      for (int i = 0; i < 8; ++i) {
+        const unsigned lo = (x0[i >> 1] >> (16 * (i & 1))) & 0xffffu;
+        const unsigned hv = (x1[i >> 1] >> (16 * (i & 1))) & 0xffffu;
+        *reinterpret_cast<unsigned*>(&sm.vt[(dc * 8 + i) * SmemBf16<D>::VSTR + pos]) =
+            lo | (hv << 16);
+      }
+    }
+    __syncthreads();
+
+    // S^T = K Q^T for two 32-key blocks.
+    f32x16 acc_s[2];
+#pragma unroll
+    for (int kb = 0; kb < 2; ++kb) {
+      acc_s[kb] = f32x16{};
+#pragma unroll
+      for (int c = 0; c < KC; ++c) {
+        const u32x4 ka = *reinterpret_cast<const u32x4*>(
+            &sm.k[(kb * 32 + qr) * SmemBf16<D>::KSTR + 16 * c + 8 * hi]);
+        acc_s[kb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(__builtin_bit_cast(bf16x8, ka),
+                                                            qreg[c], acc_s[kb], 0, 0, 0);
+      }
+    }
+
+    // Mask keys after the query (causal) and keys past the segment's end.
+    const bool need_mask = (a.causal && k0 + kBN - 1 > wq_lo) || (k0 + kBN > L);
+    if (need_mask) {
+      const int lim = a.causal ? min(tq_row, L - 1) : L - 1;
+#pragma unroll
+      for (int kb = 0; kb < 2; ++kb)
+#pragma unroll
+        for (int j = 0; j < 16; ++j) {
+          const int key = k0 + kb * 32 + 8 * (j >> 2) + 4 * hi + (j & 3);
+          if (key > lim) acc_s[kb][j] = -INFINITY;
+        }
+    }
+
+    // Online softmax for this lane's query (exp2 domain, scale folded in).
+    float mx = acc_s[0][0];
+#pragma unroll
+    for (int kb = 0; kb < 2; ++kb)
+#pragma unroll
+      for (int j = 0; j < 16; ++j) mx = fmaxf(mx, acc_s[kb][j]);
+    mx = fmaxf(mx, __shfl_xor(mx, 32));
+    const float m_new = fmaxf(m_run, mx * a.scale_log2);
+    const float alpha = __builtin_amdgcn_exp2f(m_run - m_new);
+    m_run = m_new;
+    float psum = 0.0f;
+#pragma unroll
+    for (int kb = 0; kb < 2; ++kb)
+#pragma unroll
+      for (int j = 0; j < 16; ++j) {
+        const float p = __builtin_amdgcn_exp2f(fmaf(acc_s[kb][j], a.scale_log2, -m_new));
+        acc_s[kb][j] = p;
+        psum += p;
+      }
+    l_run = fmaf(l_run, alpha, psum);
+#pragma unroll
+    for (int db = 0; db < DB; ++db)
+#pragma unroll
+      for (int j = 0; j < 16; ++j) acc_o[db][j] *= alpha;
+
+    // O^T += V^T P^T, 16 keys per MFMA step.
+#pragma unroll
+    for (int kb = 0; kb < 2; ++kb)
+#pragma unroll
+      for (int kk = 0; kk < 2; ++kk) {
+        bf16x8 pb;
+#pragma unroll
+        for (int e = 0; e < 8; ++e) pb[e] = (__bf16)acc_s[kb][8 * kk + e];
+#pragma unroll
+        for (int db = 0; db < DB; ++db) {
+          const u32x4 va = *reinterpret_cast<const u32x4*>(
+              &sm.vt[(db * 32 + qr) * SmemBf16<D>::VSTR + (kb * 2 + kk) * 16 + 8 * hi]);
+          acc_o[db] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(__builtin_bit_cast(bf16x8, va),
+                                                              pb, acc_o[db], 0, 0, 0);
+        }
+      }
+  }
+
+  // Epilogue: normalise and write this lane's row of the per-pattern output.
+  const float l_tot = l_run + __shfl_xor(l_run, 32);
+  if (!q_valid) return;
+  const float inv = 1.0f / l_tot;
+  const int64_t wrow = (int64_t)it.unit * P.lmax + tq_row;
+  float* orow = a.ws + P.o_off + wrow * D;
+#pragma unroll
+  for (int db = 0; db < DB; ++db)
+#pragma unroll
+    for (int jj = 0; jj < 4; ++jj) {
+      f32x4 o;
+#pragma unroll
+      for (int e = 0; e < 4; ++e) o[e] = acc_o[db][4 * jj + e] * inv;
+      *reinterpret_cast<f32x4*>(orow + db * 32 + 8 * jj + 4 * hi) = o;
+    }
+  if (hi == 0) a.ws[P.lse_off + wrow] = (m_run + __builtin_amdgcn_logf(l_tot)) * kLn2;
+}
+
+// ---------------------------------------------------------------------------
+// f32 VALU kernel: one thread per query row, 64 rows per work item.
+// ---------------------------------------------------------------------------
+constexpr int kBM32 = 64;
+constexpr int kBN32 = 16;
+
+template <int D>
+__global__ __launch_bounds__(kBM32) void attn_fwd_f32(AttnArgs a) {
+  __shared__ __attribute__((aligned(16))) float ks[kBN32][D];
+  __shared__ __attribute__((aligned(16))) float vs[kBN32][D];
+  Item it;
+  if (!decode_item(a, blockIdx.x, kBM32, it)) return;
+  const PatArgs& P = a.pat[it.pi];
+  const float* __restrict__ qg = static_cast<const float*>(a.q);
+  const float* __restrict__ kg = static_cast<const float*>(a.k);
+  const float* __restrict__ vg = static_cast<const float*>(a.v);
+  const int tid = threadIdx.x;
+  const int L = it.L;
+  const int q0 = it.tq * kBM32;
+  const int qend = min(q0 + kBM32, L);
+  const int t = q0 + tid;
+  const bool valid = t < L;
+
+  float qv[D], o[D];
+  {
+    const float* qp = qg + (it.row0 + (int64_t)min(t, L - 1) * it.rstride) * D;
+#pragma unroll
+    for (int d = 0; d < D; d += 4) {
+      const f32x4 x = *reinterpret_cast<const f32x4*>(qp + d);
+      qv[d] = x[0]; qv[d + 1] = x[1]; qv[d + 2] = x[2]; qv[d + 3] = x[3];
+      o[d] = o[d + 1] = o[d + 2] = o[d + 3] = 0.0f;
+    }
+  }
+  float m_run = kNegBig, l_run = 0.0f;
+  const int kv_end = a.causal ? qend : L;
+  const int lim = a.causal ? t : L - 1;
+  for (int k0 = 0; k0 < kv_end; k0 += kBN32) {
+    __syncthreads();
+    for (int task = tid; task < kBN32 * D / 4; task += kBM32) {
+      const int key = task / (D / 4);
+      const int dc = (task % (D / 4)) * 4;
+      const int tk = k0 + key;
+      f32x4 xk = f32x4{0, 0, 0, 0}, xv = f32x4{0, 0, 0, 0};
+      if (tk < L) {
+        const int64_t off = (it.row0 + (int64_t)tk * it.rstride) * D + dc;
+        xk = *reinterpret_cast<const f32x4*>(kg + off);
+        xv = *reinterpret_cast<const f32x4*>(vg + off);
+      }
+      *reinterpret_cast<f32x4*>(&ks[key][dc]) = xk;
+      *reinterpret_cast<f32x4*>(&vs[key][dc]) = xv;
+    }
+    __syncthreads();
+    float s[kBN32];
+    float mx = -INFINITY;
+#pragma unroll
+    for (int j = 0; j < kBN32; ++j) {
+      float acc = 0.0f;
+#pragma unroll
+      for (int d = 0; d < D; ++d) acc = fmaf(qv[d], ks[j][d], acc);
+      s[j] = (k0 + j <= lim) ? acc : -INFINITY;
+      mx = fmaxf(mx, s[j]);
+    }
+    const float m_new = fmaxf(m_run, mx * a.scale_log2);
+    const float alpha = __builtin_amdgcn_exp2f(m_run - m_new);
+    m_run = m_new;
+    float psum = 0.0f;
+#pragma unroll
+    for (int j = 0; j < kBN32; ++j) {
+      s[j] = __builtin_amdgcn_exp2f(fmaf(s[j], a.scale_log2, -m_new));
+      psum += s[j];
+    }
+    l_run = fmaf(l_run, alpha, psum);
+#pragma unroll
+    for (int d = 0; d < D; ++d) {
+      float acc = o[d] * alpha;
+#pragma unroll
+      for (int j = 0; j < kBN32; ++j) acc = fmaf(s[j], vs[j][d], acc);
+      o[d] = acc;
+    }
+  }
+  if (!valid) return;
+  const float inv = 1.0f / l_run;
+  const int64_t wrow = (int64_t)it.unit * P.lmax + t;
+  float* orow = a.ws + P.o_off + wrow * D;
+#pragma unroll
+  for (int d = 0; d < D; d += 4)
+    *reinterpret_cast<f32x4*>(orow + d) = f32x4{o[d] * inv, o[d + 1] * inv, o[d + 2] * inv, o[d + 3] * inv};
+  a.ws[P.lse_off + wrow] = (m_run + __builtin_amdgcn_logf(l_run)) * kLn2;
+}
+
+}  // namespace
+
+hipError_t launch_attention(const Plan& plan, const void* q, const void* k, const void* v,
+                            void* workspace, hipStream_t stream) {
+  AttnArgs a;
+  a.q = q;
+  a.k = k;
+  a.v = v;
+  a.ws = static_cast<float*>(workspace);
+  a.B = static_cast<int32_t>(plan.B);
+  a.N = static_cast<int32_t>(plan.N);
+  a.H = static_cast<int32_t>(plan.H);
+  a.npat = plan.npat;
+  a.causal = plan.causal;
+  a.total_items = static_cast<int32_t>(plan.total_items);
+  a.scale_log2 = plan.scale * kLog2e;
+  for (int i = 0; i < DA_MAX_PATTERNS; ++i) {
+    PatArgs& pa = a.pat[i];
+    if (i < plan.npat) {
+      const PatternPlan& pp = plan.pat[i];
+      pa.w = static_cast<int32_t>(pp.w);
+      pa.r = static_cast<int32_t>(pp.r);
+      pa.nseg = static_cast<int32_t>(pp.nseg);
+      pa.lmax = static_cast<int32_t>(pp.lmax);
+      pa.ntiles = static_cast<int32_t>(pp.ntiles);
+      pa.item_begin = static_cast<int32_t>(pp.item_begin);
+      pa.o_off = static_cast<int64_t>(pp.o_off / 4);
+      pa.lse_off = static_cast<int64_t>(pp.lse_off / 4);
+    } else {
+      pa = PatArgs{1, 1, 1, 1, 1, INT32_MAX, 0, 0};
+    }
+  }
+  if (plan.total_items == 0) return hipSuccess;
+  const dim3 grid(static_cast<unsigned>(plan.total_items));
+  if (plan.dtype == DA_BF16) {
+    switch (plan.D) {
+      case 32: hipLaunchKernelGGL(attn_fwd_bf16<32>, grid, dim3(kThreads), 0, stream, a); break;
+      case 64: hipLaunchKernelGGL(attn_fwd_bf16<64>, grid, dim3(kThreads), 0, stream, a); break;
+      case 128: hipLaunchKernelGGL(attn_fwd_bf16<128>, grid, dim3(kThreads), 0, stream, a); break;
+      default: return hipErrorInvalidValue;
+    }
+  } else {
+    switch (plan.D) {
+      case 32: hipLaunchKernelGGL(attn_fwd_f32<32>, grid, dim3(kBM32), 0, stream, a); break;
+      case 64: hipLaunchKernelGGL(attn_fwd_f32<64>, grid, dim3(kBM32), 0, stream, a); break;
+      case 128: hipLaunchKernelGGL(attn_fwd_f32<128>, grid, dim3(kBM32), 0, stream, a); break;
+      default: return hipErrorInvalidValue;
+    }
+  }
+  return hipGetLastError();
+}
+
+}  // namespace da

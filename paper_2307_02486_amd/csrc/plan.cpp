@@ -1,0 +1,112 @@
+// Host-side plan of a dilated-attention forward call (see plan.h).
+#include "plan.h"
+
+#include <cmath>
+#include <cstring>
+
+namespace da {
+
+FastDiv make_fastdiv(uint32_t d) {
+  FastDiv f;
+  f.d = d;
+  uint32_t l = 0;
+  while ((uint64_t{1} << l) < d) ++l;           // l = ceil(log2 d)
+  f.shift = 31 + l;
+  const uint64_t num = uint64_t{1} << f.shift;  // 2^(31+l) <= 2^62
+  f.mul = static_cast<uint32_t>((num + d - 1) / d);
+  return f;
+}
+
+int block_m_for(int dtype) { return dtype == DA_BF16 ? 128 : 64; }
+
+namespace {
+
+constexpr uint64_t kAlign = 256;
+
+uint64_t align_up(uint64_t x) { return (x + kAlign - 1) / kAlign * kAlign; }
+
+}  // namespace
+
+int make_plan(int64_t B, int64_t N, int64_t H, int64_t D, const da_pattern_t* patterns,
+              int64_t num_patterns, int64_t causal, int64_t dtype, float softmax_scale,
+              Plan* out) {
+  if (!patterns || !out) return DA_EINVAL;
+  if (B < 1 || N < 1 || H < 1 || D < 1) return DA_EINVAL;
+  if (N + H >= (int64_t{1} << 31) || H >= (int64_t{1} << 16) || B >= (int64_t{1} << 31))
+    return DA_EINVAL;
+  if (num_patterns < 1 || num_patterns > DA_MAX_PATTERNS) return DA_EINVAL;
+  if (!(softmax_scale >= 0.0f) || std::isinf(softmax_scale)) return DA_EINVAL;
+  if (causal != 0 && causal != 1) return DA_EINVAL;
+  for (int64_t i = 0; i < num_patterns; ++i) {
+    const int64_t w = patterns[i].w, r = patterns[i].r;
+    if (w < 1 || r < 1 || r > w) return DA_EINVAL;
+  }
+  if (dtype != DA_F32 && dtype != DA_BF16) return DA_EUNSUPPORTED;
+  if (D != 32 && D != 64 && D != 128) return DA_EUNSUPPORTED;
+  // every row offset ((b*N + p)*H + h) must fit in 63 bits with room to spare
+  if (static_cast<double>(B) * N * H * D > 4.0e18) return DA_EINVAL;
+
+  Plan p;
+  std::memset(&p, 0, sizeof(p));
+  p.B = B;
+  p.N = N;
+  p.H = H;
+  p.D = D;
+  p.causal = static_cast<int>(causal);
+  p.dtype = static_cast<int>(dtype);
+  p.scale = softmax_scale > 0.0f ? softmax_scale : static_cast<float>(1.0 / std::sqrt(double(D)));
+  p.npat = static_cast<int>(num_patterns);
+  p.block_m = block_m_for(p.dtype);
+  const int64_t esize = dtype == DA_BF16 ? 2 : 4;
+
+  uint64_t ws = 0;
+  int64_t items = 0;
+  long double pairs = 0.0L;
+  int64_t covered = 0;
+  for (int i = 0; i < p.npat; ++i) {
+    PatternPlan& pp = p.pat[i];
+    pp.w = patterns[i].w < N ? patterns[i].w : N;
+    // A dilation beyond N + H keeps exactly the rows it would keep at N + H:
+    // every head's offset is its own index and each segment keeps one row.
+    pp.r = patterns[i].r < N + H ? patterns[i].r : N + H;
+    pp.nseg = (N + pp.w - 1) / pp.w;
+    pp.lmax = (pp.w + pp.r - 1) / pp.r;
+    pp.ntiles = (pp.lmax + p.block_m - 1) / p.block_m;
+    pp.units = B * H * pp.nseg;
+    pp.item_begin = items;
+    items += pp.units * pp.ntiles;
+    const uint64_t rows = static_cast<uint64_t>(pp.units) * static_cast<uint64_t>(pp.lmax);
+    pp.o_off = ws;
+    ws = align_up(ws + rows * static_cast<uint64_t>(D) * 4);
+    pp.lse_off = ws;
+    ws = align_up(ws + rows * 4);
+
+    // exact kept rows and unmasked pairs: full segments, then the short tail
+    const int64_t nfull = N / pp.w;
+    const int64_t tail = N - nfull * pp.w;
+    const int64_t nres = pp.r < H ? pp.r : H;  // offsets actually used by heads
+    for (int64_t s = 0; s < nres; ++s) {
+      const int64_t heads = H / pp.r + (s < H % pp.r ? 1 : 0);  // heads with h mod r == s
+      const int64_t Lf = kept_rows(pp.w, s, pp.r);
+      const int64_t Lt = tail > 0 ? kept_rows(tail, s, pp.r) : 0;
+      covered += B * heads * (nfull * Lf + Lt);
+      const long double pf = causal ? 0.5L * Lf * (Lf + 1) : (long double)Lf * Lf;
+      const long double pt = causal ? 0.5L * Lt * (Lt + 1) : (long double)Lt * Lt;
+      pairs += (long double)B * heads * (nfull * pf + pt);
+    }
+  }
+  if (items >= (int64_t{1} << 31)) return DA_EINVAL;
+  // the combine stage launches one workgroup per 8..32 positions of each (b, h)
+  if ((N + 7) / 8 * B * H >= (int64_t{1} << 31)) return DA_EINVAL;
+  p.total_items = items;
+  p.workspace_bytes = ws;
+  p.covered_rows = covered;
+  p.sparse_flops = static_cast<double>(4.0L * D * pairs);
+  p.bytes_attn = static_cast<double>(covered) * (3.0 * D * esize + (D + 1) * 4.0);
+  p.bytes_combine = static_cast<double>(covered) * (D + 1) * 4.0 +
+                    static_cast<double>(B) * N * H * (D * esize + 4.0);
+  *out = p;
+  return DA_OK;
+}
+
+}  // namespace da

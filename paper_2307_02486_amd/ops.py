@@ -1,0 +1,114 @@
+"""Python entry points of the dilated-attention forward pass.
+
+`plan` and `dilated_attn` mirror the C ABI (dilated_attn_plan /
+dilated_attn_fwd): torch supplies device memory and the stream, every step of
+the computation runs in the HIP kernels of libdilated_attn.so.
+"""
+from __future__ import annotations
+
+import ctypes
+from typing import Sequence, Tuple
+
+import torch
+
+from . import _lib
+
+_DTYPES = {torch.float32: _lib.DA_F32, torch.bfloat16: _lib.DA_BF16}
+
+
+def _dtype_code(dtype) -> int:
+    if dtype not in _DTYPES:
+        raise TypeError(f"unsupported dtype {dtype}; use float32 or bfloat16")
+    return _DTYPES[dtype]
+
+
+def plan(B: int, N: int, H: int, D: int, patterns: Sequence[Tuple[int, int]], causal: bool = True,
+         dtype=torch.bfloat16, scale: float | None = None) -> dict:
+    """Validate a problem and return its workspace size and work counts (host only)."""
+    lib = _lib.load()
+    arr, n = _lib.pattern_array(patterns)
+    info = _lib.PlanInfo()
+    rc = lib.dilated_attn_plan(B, N, H, D, arr, n, int(bool(causal)), _dtype_code(dtype),
+                               float(scale or 0.0), ctypes.byref(info))
+    if rc != 0:
+        raise _lib.DilatedAttnError(rc, lib)
+    return {k: getattr(info, k) for k, _ in _lib.PlanInfo._fields_}
+
+
+def plan_raw(B, N, H, D, patterns, causal, dtype_code, scale):
+    """Call dilated_attn_plan with raw integer arguments; return (rc, info dict)."""
+    lib = _lib.load()
+    arr, n = _lib.pattern_array(patterns)
+    info = _lib.PlanInfo()
+    rc = lib.dilated_attn_plan(B, N, H, D, arr, n, causal, dtype_code, scale, ctypes.byref(info))
+    return rc, {k: getattr(info, k) for k, _ in _lib.PlanInfo._fields_}
+
+
+def workspace_for(q: torch.Tensor, patterns, causal=True, scale=None) -> torch.Tensor:
+    """Allocate (with torch) the device workspace a call on q's shape needs."""
+    B, N, H, D = q.shape
+    info = plan(B, N, H, D, patterns, causal, q.dtype, scale)
+    return torch.empty(max(256, int(info["workspace_bytes"])), dtype=torch.uint8, device=q.device)
+
+
+def dilated_attn(q: torch.Tensor, k: torch.Tensor, v: torch.Tensor,
+                 patterns: Sequence[Tuple[int, int]], causal: bool = True,
+                 scale: float | None = None, out: torch.Tensor | None = None,
+                 lse: torch.Tensor | None = None, workspace: torch.Tensor | None = None,
+                 stream: torch.cuda.Stream | None = None):
+    """Dilated-attention forward.  q, k, v: [B, N, H, D] contiguous on the GPU.
+
+    Returns (out [B,N,H,D] in q's dtype, lse [B,H,N] float32).  Work is
+    enqueued on `stream` (default: torch's current stream) and not waited for.
+    """
+    lib = _lib.load()
+    if q.device.type != "cuda":
+        raise RuntimeError("dilated_attn runs on the GPU only; q must be a device tensor")
+    for t in (q, k, v):
+        if not t.is_contiguous() or t.shape != q.shape or t.dtype != q.dtype or t.device != q.device:
+            raise ValueError("q, k, v must be contiguous tensors of the same shape, dtype and device")
+    if q.dim() != 4:
+        raise ValueError("q, k, v must be [B, N, H, D]")
+    B, N, H, D = q.shape
+    if out is None:
+        out = torch.empty_like(q)
+    if lse is None:
+        lse = torch.empty((B, H, N), dtype=torch.float32, device=q.device)
+    if workspace is None:
+        workspace = workspace_for(q, patterns, causal, scale)
+    if stream is None:
+        stream = torch.cuda.current_stream(q.device)
+    arr, n = _lib.pattern_array(patterns)
+    rc = lib.dilated_attn_fwd(q.data_ptr(), k.data_ptr(), v.data_ptr(), out.data_ptr(), lse.data_ptr(),
+                              B, N, H, D, arr, n, int(bool(causal)), _dtype_code(q.dtype),
+                              float(scale or 0.0), workspace.data_ptr(), workspace.numel(),
+                              stream.cuda_stream)
+    if rc != 0:
+        raise _lib.DilatedAttnError(rc, lib)
+    return out, lse
+
+
+class StageTimer:
+    """Context manager around dilated_attn_profile_begin/end: per-stage HIP
+    event timing of the calls made inside it (on each call's own stream)."""
+
+    def __init__(self, capacity: int = 4096):
+        self.capacity = capacity
+        self.ms_attention = self.ms_combine = 0.0
+        self.calls = 0
+
+    def __enter__(self):
+        lib = _lib.load()
+        rc = lib.dilated_attn_profile_begin(self.capacity)
+        if rc != 0:
+            raise _lib.DilatedAttnError(rc, lib)
+        return self
+
+    def __exit__(self, *exc):
+        lib = _lib.load()
+        a, c, n = ctypes.c_double(), ctypes.c_double(), ctypes.c_int64()
+        rc = lib.dilated_attn_profile_end(ctypes.byref(a), ctypes.byref(c), ctypes.byref(n))
+        if rc != 0 and exc[0] is None:
+            raise _lib.DilatedAttnError(rc, lib)
+        self.ms_attention, self.ms_combine, self.calls = a.value, c.value, n.value
+        return False

@@ -1,0 +1,156 @@
+"""Host-side logic: plan helpers built with g++ (also under ASan/UBSan), the
+C ABI's exported symbols, plan accounting and argument errors.  No GPU."""
+import ctypes
+import math
+import os
+import re
+import shutil
+import subprocess
+
+import numpy as np
+import pytest
+import torch
+
+import oracle
+import workloads
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+CSRC = os.path.join(ROOT, "paper_2307_02486_amd", "csrc")
+HEADER = os.path.join(ROOT, "include", "dilated_attn.h")
+
+
+def _gxx_run(tmp_path, extra):
+    gxx = shutil.which("g++")
+    if gxx is None:
+        pytest.skip("g++ not available")
+    exe = str(tmp_path / "t")
+    cmd = [gxx, "-std=c++17", "-O1", *extra, "-I", CSRC, "-I", os.path.join(ROOT, "include"),
+           os.path.join(ROOT, "tests", "cpp", "test_plan_host.cpp"), os.path.join(CSRC, "plan.cpp"), "-o", exe]
+    subprocess.run(cmd, check=True)
+    res = subprocess.run([exe], capture_output=True, text=True, timeout=120)
+    assert res.returncode == 0, res.stdout + res.stderr
+    assert "OK" in res.stdout
+
+
+def test_plan_helpers_host(tmp_path):
+    _gxx_run(tmp_path, [])
+
+
+def test_plan_helpers_sanitized(tmp_path):
+    _gxx_run(tmp_path, ["-fsanitize=address,undefined", "-fno-sanitize-recover=all", "-g"])
+
+
+@pytest.fixture(scope="module")
+def lib():
+    from paper_2307_02486_amd import _lib
+    return _lib.load()
+
+
+def test_exports_every_declared_symbol(lib):
+    text = open(HEADER).read()
+    names = re.findall(r"^\s*(?:const\s+)?\w+\*?\s+\*?(dilated_attn_\w+)\s*\(", text, re.M)
+    assert set(names) == {"dilated_attn_plan", "dilated_attn_fwd", "dilated_attn_strerror",
+                          "dilated_attn_profile_begin", "dilated_attn_profile_end"}
+    for n in names:
+        assert hasattr(lib, n), n
+    nm = subprocess.run(["nm", "-D", "--defined-only", os.path.join(ROOT, "paper_2307_02486_amd",
+                                                                     "libdilated_attn.so")],
+                        capture_output=True, text=True).stdout
+    for n in names:
+        assert re.search(rf"\bT {n}$", nm, re.M), n
+
+
+def test_strerror(lib):
+    for code in (0, -1, -2, -3, -4, -5, 7):
+        assert lib.dilated_attn_strerror(code)
+
+
+@pytest.mark.parametrize("wl", workloads.WORKLOADS, ids=lambda w: w.name)
+def test_plan_accounting_matches_enumeration(wl):
+    from paper_2307_02486_amd import plan
+    info = plan(wl.B, wl.N, wl.H, wl.D, wl.patterns, wl.causal, wl.torch_dtype)
+    flops = oracle.sparse_flops(wl.B, wl.N, wl.H, wl.D, wl.patterns, wl.causal)
+    rows = wl.B * oracle.covered_rows(wl.N, wl.H, wl.patterns)
+    assert info["covered_rows"] == rows
+    assert info["sparse_flops"] == pytest.approx(flops, rel=1e-12)
+    es = 2 if wl.dtype == "bf16" else 4
+    assert info["bytes_attn"] == rows * (3 * wl.D * es + 4 * (wl.D + 1))
+    assert info["bytes_combine"] == rows * 4 * (wl.D + 1) + wl.B * wl.N * wl.H * (wl.D * es + 4)
+
+
+def test_plan_accounting_random_small():
+    from paper_2307_02486_amd import plan
+    rng = np.random.default_rng(7)
+    for _ in range(150):
+        N = int(rng.integers(1, 300))
+        H = int(rng.integers(1, 9))
+        pats = []
+        for _ in range(int(rng.integers(1, 6))):
+            w = int(rng.integers(1, 2 * N + 3))
+            pats.append((w, int(rng.integers(1, w + 1))))
+        causal = bool(rng.random() < 0.6)
+        info = plan(1, N, H, 32, pats, causal, torch.float32)
+        assert info["covered_rows"] == oracle.covered_rows(N, H, pats)
+        assert info["sparse_flops"] == oracle.sparse_flops(1, N, H, 32, pats, causal)
+
+
+def test_plan_paper_flop_formula():
+    """Sec. 2.4: 2*N*d*sum(w/r^2) per head, plus 2*d per kept row (diagonal)."""
+    from paper_2307_02486_amd import plan
+    wl = workloads.BY_NAME["n256k_h16_d64_8pat_geo"]
+    info = plan(wl.B, wl.N, wl.H, wl.D, wl.patterns)
+    paper = wl.H * 2 * wl.N * wl.D * sum(w / r ** 2 for w, r in wl.patterns)
+    assert info["sparse_flops"] == pytest.approx(paper + 2 * wl.D * info["covered_rows"], rel=1e-12)
+    # geometric bound with alpha = 2, w0 = 2048
+    assert info["sparse_flops"] - 2 * wl.D * info["covered_rows"] <= wl.H * 4 * 2048 * wl.N * wl.D
+
+
+BAD_PLANS = [
+    # (B, N, H, D, patterns, causal, dtype, scale) -> code
+    ((0, 16, 2, 64, [(8, 1)], 1, 1, 0.0), "DA_EINVAL"),
+    ((1, 0, 2, 64, [(8, 1)], 1, 1, 0.0), "DA_EINVAL"),
+    ((1, 16, 0, 64, [(8, 1)], 1, 1, 0.0), "DA_EINVAL"),
+    ((1, 16, 2, 64, [], 1, 1, 0.0), "DA_EINVAL"),
+    ((1, 16, 2, 64, [(8, 1)] * 17, 1, 1, 0.0), "DA_EINVAL"),
+    ((1, 16, 2, 64, [(8, 9)], 1, 1, 0.0), "DA_EINVAL"),
+    ((1, 16, 2, 64, [(8, 0)], 1, 1, 0.0), "DA_EINVAL"),
+    ((1, 16, 2, 64, [(0, 1)], 1, 1, 0.0), "DA_EINVAL"),
+    ((1, 16, 2, 64, [(8, 1)], 2, 1, 0.0), "DA_EINVAL"),
+    ((1, 16, 2, 64, [(8, 1)], 1, 1, -1.0), "DA_EINVAL"),
+    ((1, 16, 2, 64, [(8, 1)], 1, 1, float("nan")), "DA_EINVAL"),
+    ((1, 2 ** 31, 2, 64, [(8, 1)], 1, 1, 0.0), "DA_EINVAL"),
+    ((1, 16, 2, 48, [(8, 1)], 1, 1, 0.0), "DA_EUNSUPPORTED"),
+    ((1, 16, 2, 64, [(8, 1)], 1, 7, 0.0), "DA_EUNSUPPORTED"),
+]
+
+
+@pytest.mark.parametrize("args,code", BAD_PLANS)
+def test_plan_rejects(args, code):
+    from paper_2307_02486_amd import _lib, plan_raw
+    rc, _ = plan_raw(*args)
+    assert _lib.ERRORS[rc] == code
+
+
+def test_fwd_rejects_before_touching_device(lib):
+    """Argument errors return before any HIP call (fake, never dereferenced pointers)."""
+    from paper_2307_02486_amd import _lib
+    arr, n = _lib.pattern_array([(8, 1)])
+    good = [0x10000, 0x20000, 0x30000, 0x40000, 0x50000]
+    def call(ptrs, ws=0x100000, ws_bytes=1 << 20, B=1, N=16, H=2, D=64, dtype=1, pats=(arr, n)):
+        return lib.dilated_attn_fwd(*ptrs, B, N, H, D, pats[0], pats[1], 1, dtype, 0.0, ws, ws_bytes, None)
+    assert _lib.ERRORS[call([0] + good[1:])] == "DA_EINVAL"
+    assert _lib.ERRORS[call(good, ws=0)] == "DA_EINVAL"
+    assert _lib.ERRORS[call([good[0] + 8] + good[1:])] == "DA_EALIGN"
+    assert _lib.ERRORS[call(good, ws=0x100008)] == "DA_EALIGN"
+    assert _lib.ERRORS[call(good, ws_bytes=16)] == "DA_EWORKSPACE"
+    assert _lib.ERRORS[call([good[0], good[1], good[2], good[0], good[4]])] == "DA_EINVAL"   # out aliases q
+    assert _lib.ERRORS[call(good, ws=good[1])] == "DA_EINVAL"                               # workspace aliases k
+    assert _lib.ERRORS[call(good, D=40)] == "DA_EUNSUPPORTED"
+    bad_arr, bn = _lib.pattern_array([(4, 5)])
+    assert _lib.ERRORS[call(good, pats=(bad_arr, bn))] == "DA_EINVAL"
+
+
+def test_profile_window_arguments(lib):
+    assert lib.dilated_attn_profile_begin(0) == -1
+    assert lib.dilated_attn_profile_begin(1 << 21) == -1
+    assert lib.dilated_attn_profile_end(None, None, None) == -1   # no window open

@@ -1,0 +1,163 @@
+"""GPU parity: the HIP path against the CPU oracle on the same seeded inputs.
+
+Bars: bf16 inputs max-abs 2e-2 on out and 1e-2 on lse; float32 inputs 1e-4.
+The oracle sees the exact float64 values of the tensors handed to the GPU.
+"""
+import math
+
+import numpy as np
+import pytest
+import torch
+
+import oracle
+import workloads
+from tests.gpu_util import (TOL, compare_full, compare_rows, note, require_gpu, run_gpu,
+                            sample_rows, to64)
+
+pytestmark = pytest.mark.gpu
+
+
+@pytest.fixture(scope="module", autouse=True)
+def _gpu():
+    require_gpu()
+
+
+# ---- the workloads -----------------------------------------------------------
+
+@pytest.mark.parametrize("name", ["tiny_n256_h2_d32_f32", "n8k_b2_h12_d64_3pat"])
+def test_workload_all_rows(name):
+    wl = workloads.BY_NAME[name]
+    note(f"[parity] {name} all rows")
+    q, k, v = workloads.make_qkv(wl, device="cuda")
+    eo, el = compare_full(q, k, v, list(wl.patterns), wl.causal, wl.dtype, tag=name)
+    note(f"[parity] {name}: out err {eo:.3e} lse err {el:.3e}")
+
+
+def test_n32k_all_rows_of_two_heads():
+    """The benchmark workload: every row of head 0 (segment lengths 2731) and
+    head 5 (2730 for the r = 6 and r = 12 patterns)."""
+    wl = workloads.BY_NAME["n32k_h12_d64_5pat"]
+    note("[parity] n32k heads 0,5 all rows")
+    q, k, v = workloads.make_qkv(wl, device="cuda")
+    eo, el = compare_full(q, k, v, list(wl.patterns), wl.causal, wl.dtype, tag=wl.name, heads=[0, 5])
+    note(f"[parity] n32k heads 0,5: out err {eo:.3e} lse err {el:.3e}")
+
+
+@pytest.mark.parametrize("name", ["n32k_h12_d64_5pat", "n256k_h16_d64_8pat_geo", "n1m_h16_d128_6pat"])
+def test_workload_sampled_rows(name):
+    wl = workloads.BY_NAME[name]
+    note(f"[parity] {name} sampled rows")
+    q, k, v = workloads.make_qkv(wl, device="cuda")
+    out, lse = run_gpu(q, k, v, list(wl.patterns), wl.causal)
+    # every row written, none NaN/Inf (all rows are covered: the first pattern has r = 1)
+    assert torch.isfinite(lse).all().item()
+    assert torch.isfinite(out).all().item()
+    rows = sample_rows(wl, np.random.default_rng(wl.seed), per_head=48)
+    eo, el = compare_rows(q, k, v, out, lse, wl, rows, tag=name)
+    note(f"[parity] {name}: {len(rows)} rows, out err {eo:.3e} lse err {el:.3e}")
+
+
+# ---- edge cases at small sizes ------------------------------------------------
+
+EDGE = [
+    # (B, N, H, D, dtype, patterns, causal)
+    (1, 1, 1, 64, "bf16", [(1, 1)], True),
+    (1, 1, 3, 32, "f32", [(4, 2)], True),
+    (1, 300, 3, 64, "bf16", [(128, 1), (300, 3), (64, 5)], True),
+    (2, 777, 5, 32, "bf16", [(256, 1), (512, 7), (1000, 9)], False),
+    (1, 513, 17, 128, "bf16", [(512, 1), (513, 20)], True),
+    (1, 200, 2, 64, "bf16", [(50, 3)], True),            # rows no pattern keeps
+    (1, 256, 4, 64, "bf16", [(64, 1), (64, 1), (256, 4)], True),   # duplicate pattern
+    (1, 1000, 2, 64, "bf16", [(1000, 1)], True),         # dense: 8 query tiles, ragged
+    (1, 1000, 2, 64, "bf16", [(1000, 1)], False),
+    (1, 1031, 6, 64, "bf16", [(2048, 1), (4096, 3), (333, 2)], True),  # w > N
+    (2, 129, 3, 64, "f32", [(64, 1), (129, 2), (100, 7)], True),
+    (1, 300, 2, 128, "f32", [(128, 1), (300, 3)], False),
+    (1, 160, 2, 32, "f32", [(160, 1)], True),
+    (1, 4096, 2, 128, "bf16", [(4096, 1), (2048, 2)], True),
+    (1, 64, 16, 64, "bf16", [(64, 64), (64, 1)], True),   # r = w
+]
+
+
+@pytest.mark.parametrize("case", EDGE, ids=lambda c: f"B{c[0]}N{c[1]}H{c[2]}D{c[3]}{c[4]}{'c' if c[6] else 'nc'}{len(c[5])}p")
+def test_edge_cases(case):
+    B, N, H, D, dt, pats, causal = case
+    note(f"[edge] {case}")
+    dtype = torch.bfloat16 if dt == "bf16" else torch.float32
+    seed = 1000 + N * 7 + H * 13 + D
+    q, k, v = (workloads.make_random((B, N, H, D), dtype, 1.0, seed, "cuda", t) for t in range(3))
+    compare_full(q, k, v, pats, causal, dt, tag=str(case))
+
+
+@pytest.mark.parametrize("dt", ["bf16", "f32"])
+def test_q_zero_closed_form(dt):
+    """q = 0: lse = ln(count of visible keys over all patterns), out = their mean."""
+    B, N, H, D = 1, 333, 4, 64
+    pats = [(64, 1), (128, 3), (333, 5)]
+    dtype = torch.bfloat16 if dt == "bf16" else torch.float32
+    note(f"[q0] {dt}")
+    q = torch.zeros((B, N, H, D), dtype=dtype, device="cuda")
+    k = workloads.make_random((B, N, H, D), dtype, 1.0, 77, "cuda", 1)
+    v = workloads.make_random((B, N, H, D), dtype, 1.0, 77, "cuda", 2)
+    out, lse = run_gpu(q, k, v, pats, True)
+    v64 = to64(v)
+    go, gl = to64(out), to64(lse)
+    for h in range(H):
+        for p in range(N):
+            cnt, acc = 0, np.zeros(D)
+            for (w, r) in pats:
+                st = (p // w) * w
+                if (p - st) % r != h % r:
+                    continue
+                prefix = list(range(st + h % r, p + 1, r))
+                cnt += len(prefix)
+                acc += v64[0, prefix, h].sum(axis=0)
+            assert abs(gl[0, h, p] - math.log(cnt)) < 1e-5
+            assert np.abs(go[0, p, h] - acc / cnt).max() < TOL[dt][0]
+
+
+def test_scale_argument():
+    B, N, H, D = 1, 200, 2, 64
+    q, k, v = (workloads.make_random((B, N, H, D), torch.bfloat16, 1.0, 5, "cuda", t) for t in range(3))
+    note("[scale]")
+    compare_full(q, k, v, [(64, 1), (200, 2)], True, "bf16", scale=0.3, tag="scale=0.3")
+
+
+def test_deterministic():
+    wl = workloads.BY_NAME["n8k_b2_h12_d64_3pat"]
+    note("[determinism] n8k")
+    q, k, v = workloads.make_qkv(wl, device="cuda")
+    o1, l1 = run_gpu(q, k, v, list(wl.patterns))
+    o2, l2 = run_gpu(q, k, v, list(wl.patterns))
+    assert torch.equal(o1, o2) and torch.equal(l1, l2)
+
+
+def test_error_leaves_buffers_untouched():
+    from paper_2307_02486_amd import DilatedAttnError, dilated_attn
+    q, k, v = (workloads.make_random((1, 64, 2, 64), torch.bfloat16, 1.0, 9, "cuda", t) for t in range(3))
+    out = torch.full_like(q, 7.0)
+    lse = torch.full((1, 2, 64), 7.0, device="cuda")
+    ws = torch.empty(16, dtype=torch.uint8, device="cuda")
+    note("[errors]")
+    with pytest.raises(DilatedAttnError) as e:
+        dilated_attn(q, k, v, [(32, 1)], out=out, lse=lse, workspace=ws)
+    assert e.value.name == "DA_EWORKSPACE"
+    with pytest.raises(DilatedAttnError) as e:
+        dilated_attn(q, k, v, [(32, 33)], out=out, lse=lse)
+    assert e.value.name == "DA_EINVAL"
+    torch.cuda.synchronize()
+    assert (out == 7.0).all().item() and (lse == 7.0).all().item()
+
+
+def test_stream_argument():
+    """Work goes to the stream given, in order with the caller's other work."""
+    from paper_2307_02486_amd import dilated_attn
+    B, N, H, D = 1, 512, 2, 64
+    q, k, v = (workloads.make_random((B, N, H, D), torch.bfloat16, 1.0, 11, "cuda", t) for t in range(3))
+    ref_o, ref_l = run_gpu(q, k, v, [(128, 1), (512, 4)])
+    s = torch.cuda.Stream()
+    note("[stream]")
+    with torch.cuda.stream(s):
+        o, l = dilated_attn(q, k, v, [(128, 1), (512, 4)], stream=s)
+    s.synchronize()
+    assert torch.equal(o, ref_o) and torch.equal(l, ref_l)
