@@ -36,7 +36,21 @@ def parse():
     ap.add_argument("--workload", default=DEFAULT_WORKLOAD)
     ap.add_argument("--cpu-seconds", type=float, default=12.0,
                     help="minimum CPU time spent on the oracle sample (0 skips the CPU baseline)")
+    ap.add_argument("--copy-calibration-mib", type=int, default=0,
+                    help="only run a plain device-to-device copy of this many MiB (5 times), to "
+                         "calibrate the HBM byte counters of a profiler against a known size")
     return ap.parse_args()
+
+
+def copy_calibration(mib):
+    """A plain copy of a known number of bytes (read mib MiB, write mib MiB)."""
+    import torch
+    x = torch.ones(mib * (1 << 20) // 4, dtype=torch.float32, device="cuda")
+    y = torch.empty_like(x)
+    for _ in range(5):
+        y.copy_(x)
+    torch.cuda.synchronize()
+    print(json.dumps({"copy_calibration_bytes_each_way": mib * (1 << 20), "launches": 5}), flush=True)
 
 
 def cpu_baseline(wl, q, k, v, min_seconds):
@@ -83,6 +97,9 @@ def main():
         print(f"bench.py: this build runs on one GPU only (asked for --gpus {args.gpus}); "
               "the sequence-parallel multi-GPU path is not built", file=sys.stderr)
         sys.exit(2)
+    if args.copy_calibration_mib > 0:
+        copy_calibration(args.copy_calibration_mib)
+        return
     import torch
 
     import workloads

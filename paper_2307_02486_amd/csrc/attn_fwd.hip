@@ -23,6 +23,7 @@ namespace da {
 namespace {
 
 typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
+typedef __bf16 bf16x2 __attribute__((ext_vector_type(2)));
 typedef float f32x16 __attribute__((ext_vector_type(16)));
 typedef float f32x4 __attribute__((ext_vector_type(4)));
 typedef unsigned int u32x4 __attribute__((ext_vector_type(4)));
@@ -33,7 +34,7 @@ constexpr float kLog2e = 1.442695040888963407f;
 constexpr float kNegBig = -1.0e30f;   // finite "minus infinity" for running maxima
 
 struct PatArgs {
-  int32_t w, r, nseg, lmax, ntiles, item_begin;
+  int32_t w, r, nseg, lmax, ntiles, units;
   int64_t o_off;    // float offset of this pattern's output rows in the workspace
   int64_t lse_off;  // float offset of this pattern's lse in the workspace
 };
@@ -61,14 +62,26 @@ struct Item {
 
 // Work items are ordered pattern by pattern; inside a pattern, unit by unit
 // (segment fastest), and inside a unit the query tiles run from the last (the
-// longest under a causal mask) to the first.
-__device__ inline bool decode_item(const AttnArgs& a, int item, int block_m, Item& it) {
+// longest under a causal mask) to the first.  Workgroups are handed to the
+// eight XCDs round-robin (launch index mod 8), so launch index x is mapped to
+// XCD c = x mod 8 and the units with index = c (mod 8) are given to that XCD:
+// the query tiles of one segment then run on one XCD, close together in time,
+// and its K/V rows are fetched into that XCD's L2 once.
+__device__ inline bool decode_item(const AttnArgs& a, int bid, int block_m, Item& it) {
+  const int c = bid & 7;
+  int slot = bid >> 3;
   int pi = 0;
-  while (pi + 1 < a.npat && item >= a.pat[pi + 1].item_begin) ++pi;
+  for (;; ++pi) {
+    if (pi >= a.npat) return false;
+    const PatArgs& P = a.pat[pi];
+    const int n = (P.units > c ? (P.units - c + 7) >> 3 : 0) * P.ntiles;
+    if (slot < n) break;
+    slot -= n;
+  }
   const PatArgs& P = a.pat[pi];
-  const int rem = item - P.item_begin;
-  const int unit = rem / P.ntiles;
-  it.tq = P.ntiles - 1 - (rem - unit * P.ntiles);
+  const int j = slot / P.ntiles;
+  const int unit = c + 8 * j;
+  it.tq = P.ntiles - 1 - (slot - j * P.ntiles);
   it.pi = pi;
   it.unit = unit;
   it.g = unit % P.nseg;
@@ -88,23 +101,29 @@ __device__ inline bool decode_item(const AttnArgs& a, int item, int block_m, Ite
 // bf16 MFMA kernel
 // ---------------------------------------------------------------------------
 constexpr int kBM = 128;      // query rows per work item
-constexpr int kBN = 64;       // keys per K/V tile
 constexpr int kThreads = 256; // four waves
+// A row's running max is raised only when a tile's max exceeds it by more than
+// this (log2 units); until then probabilities may reach 2^kRescaleSlack, which
+// bf16 and the fp32 sums hold exactly as well as values below 1.
+constexpr float kRescaleSlack = 8.0f;
 
-// Position of key `key` (0..kBN-1) inside a transposed V row: within each group
-// of 16 keys, keys {0-3, 8-11} come first and {4-7, 12-15} second, which is the
+// Keys per K/V tile for a head dim: 128 where the registers allow it.
+template <int D> struct KeyTile { static constexpr int value = D <= 64 ? 128 : 64; };
+
+// Position of key `key` inside a transposed V row: within each group of 16
+// keys, keys {0-3, 8-11} come first and {4-7, 12-15} second, which is the
 // order in which the upper and lower half-waves hold them after S^T.
 __device__ inline int vt_pos(int key) {
   const int k16 = key & 15;
   return (key & ~15) | (((k16 >> 2) & 1) << 3) | ((k16 >> 3) << 2) | (k16 & 3);
 }
 
-template <int D>
+template <int D, int BN>
 struct SmemBf16 {
-  static constexpr int KSTR = D + 8;    // row pitch (elements) of the K tile
-  static constexpr int VSTR = kBN + 8;  // row pitch (elements) of the V^T tile
-  u16 k[kBN * KSTR];
-  u16 vt[D * VSTR];
+  static constexpr int KSTR = D + 8;    // row pitch (elements) of a K tile
+  static constexpr int VSTR = BN + 8;   // row pitch (elements) of a V^T tile
+  u16 k[2][BN * KSTR];                  // double-buffered
+  u16 vt[2][D * VSTR];
 };
 
 __device__ inline u32x4 load16(const u16* p) { return *reinterpret_cast<const u32x4*>(p); }
@@ -112,16 +131,20 @@ __device__ inline u32x4 load16(const u16* p) { return *reinterpret_cast<const u3
 template <int D>
 __global__ __launch_bounds__(kThreads) void attn_fwd_bf16(AttnArgs a) {
   static_assert(D % 32 == 0, "head dim must be a multiple of 32");
+  constexpr int BN = KeyTile<D>::value;
   constexpr int KC = D / 16;  // MFMA k-steps over the head dim
   constexpr int DB = D / 32;  // 32-wide blocks of the head dim in O^T
-  __shared__ __attribute__((aligned(16))) SmemBf16<D> sm;
+  constexpr int SB = BN / 32; // 32-key blocks of S^T per tile
+  constexpr int KT = BN * D / 8 / kThreads;                 // 16-B K chunks per thread per tile
+  constexpr int VTASKS = (BN / 2) * (D / 8);                // (key pair, 8-wide chunk) V tasks
+  constexpr int VT = (VTASKS + kThreads - 1) / kThreads;    // V tasks per thread
+  using Smem = SmemBf16<D, BN>;
+  __shared__ __attribute__((aligned(16))) Smem sm;
 
   Item it;
   if (!decode_item(a, blockIdx.x, kBM, it)) return;
   const PatArgs& P = a.pat[it.pi];
   const u16* __restrict__ qg = static_cast<const u16*>(a.q);
-  const u16* __restrict__ kg = static_cast<const u16*>(a.k);
-  const u16* __restrict__ vg = static_cast<const u16*>(a.v);
 
   const int tid = threadIdx.x;
   const int lane = tid & 63;
@@ -133,6 +156,7 @@ __global__ __launch_bounds__(kThreads) void attn_fwd_bf16(AttnArgs a) {
   const int qend = min(q0 + kBM, L);
   const int tq_row = q0 + wv * 32 + qr;  // this lane's query (kept-row index)
   const bool q_valid = tq_row < L;
+  const int64_t row_step = it.rstride * D;  // elements between consecutive kept rows
 
   // Q^T operand: lane holds query tq_row, head-dim slice [16c + 8hi, +8).
   bf16x8 qreg[KC];
@@ -145,119 +169,152 @@ __global__ __launch_bounds__(kThreads) void attn_fwd_bf16(AttnArgs a) {
     }
   }
 
+  // Fixed per-thread roles in the tile loads; pointers advance by BN kept rows
+  // per tile.
+  //  K chunk i: key (tid + 256i) / (D/8), head-dim chunk (tid + 256i) % (D/8)
+  //  V task i:  keys 2kp, 2kp+1 with kp = (tid + 256i) % (BN/2), chunk (tid + 256i) / (BN/2)
+  const u16* kp_[KT];
+  int kkey[KT];
+#pragma unroll
+  for (int i = 0; i < KT; ++i) {
+    const int task = tid + i * kThreads;
+    kkey[i] = task / (D / 8);
+    kp_[i] = static_cast<const u16*>(a.k) + it.row0 * D + (int64_t)kkey[i] * row_step + (task % (D / 8)) * 8;
+  }
+  const u16* vp_[VT];
+  int vkey[VT];
+#pragma unroll
+  for (int i = 0; i < VT; ++i) {
+    const int task = min(tid + i * kThreads, VTASKS - 1);
+    vkey[i] = 2 * (task % (BN / 2));
+    vp_[i] = static_cast<const u16*>(a.v) + it.row0 * D + (int64_t)vkey[i] * row_step + (task / (BN / 2)) * 8;
+  }
+  const int64_t tile_step = row_step * BN;
+
+  u32x4 rk[KT], rv0[VT], rv1[VT];
+  auto load_tile = [&](int jt) {
+    const int k0 = jt * BN;
+    const int64_t off = tile_step * jt;
+#pragma unroll
+    for (int i = 0; i < KT; ++i)
+      rk[i] = k0 + kkey[i] < L ? load16(kp_[i] + off) : u32x4{0, 0, 0, 0};
+#pragma unroll
+    for (int i = 0; i < VT; ++i) {
+      const int t = k0 + vkey[i];
+      rv0[i] = t < L ? load16(vp_[i] + off) : u32x4{0, 0, 0, 0};
+      rv1[i] = t + 1 < L ? load16(vp_[i] + off + row_step) : u32x4{0, 0, 0, 0};
+    }
+  };
+  auto store_tile = [&](int buf) {
+#pragma unroll
+    for (int i = 0; i < KT; ++i) {
+      const int task = tid + i * kThreads;
+      *reinterpret_cast<u32x4*>(&sm.k[buf][(task / (D / 8)) * Smem::KSTR + (task % (D / 8)) * 8]) = rk[i];
+    }
+#pragma unroll
+    for (int i = 0; i < VT; ++i) {
+      const int task = tid + i * kThreads;
+      if (VTASKS % kThreads == 0 || task < VTASKS) {
+        u16* dst = &sm.vt[buf][(task / (BN / 2)) * 8 * Smem::VSTR + vt_pos(2 * (task % (BN / 2)))];
+#pragma unroll
+        for (int e = 0; e < 8; ++e) {
+          // (key 2kp, key 2kp+1) of head-dim element dc*8 + e, as one 32-bit word
+          const unsigned sel = (e & 1) ? 0x07060302u : 0x05040100u;
+          *reinterpret_cast<unsigned*>(dst + e * Smem::VSTR) =
+              __builtin_amdgcn_perm(rv1[i][e >> 1], rv0[i][e >> 1], sel);
+        }
+      }
+    }
+  };
+
   f32x16 acc_o[DB];
 #pragma unroll
   for (int db = 0; db < DB; ++db) acc_o[db] = f32x16{};
-  float m_run = kNegBig;  // running max of scaled scores (log2 domain)
+  float m_run = kNegBig;  // reference max of scaled scores (log2 domain)
   float l_run = 0.0f;     // this half-wave's share of the running denominator
 
   const int kv_end = a.causal ? qend : L;
-  const int ntile = (kv_end + kBN - 1) / kBN;
+  const int ntile = (kv_end + BN - 1) / BN;
   const int wq_lo = q0 + wv * 32;  // smallest query of this wave
+  const int lim = a.causal ? min(tq_row, L - 1) : L - 1;  // last visible key of this lane
 
+  load_tile(0);
+  store_tile(0);
+  __syncthreads();
   for (int jt = 0; jt < ntile; ++jt) {
-    const int k0 = jt * kBN;
-    __syncthreads();
-    // K tile: row-major [key][d], 16-byte chunks, 8 lanes per 128-byte row.
-#pragma unroll
-    for (int task = tid; task < kBN * D / 8; task += kThreads) {
-      const int key = task / (D / 8);
-      const int dc = task % (D / 8);
-      const int t = k0 + key;
-      u32x4 x = u32x4{0, 0, 0, 0};
-      if (t < L) x = load16(kg + (it.row0 + (int64_t)t * it.rstride) * D + dc * 8);
-      *reinterpret_cast<u32x4*>(&sm.k[key * SmemBf16<D>::KSTR + dc * 8]) = x;
-    }
-    // V tile transposed: a thread takes keys (2kp, 2kp+1) of one 8-wide chunk
-    // of the head dim and writes 8 key pairs as 32-bit words.
-#pragma unroll
-    for (int task = tid; task < (kBN / 2) * (D / 8); task += kThreads) {
-      const int kp = task & 31;
-      const int dc = task >> 5;
-      const int t = k0 + 2 * kp;
-      u32x4 x0 = u32x4{0, 0, 0, 0}, x1 = u32x4{0, 0, 0, 0};
-      const u16* vp = vg + (it.row0 + (int64_t)t * it.rstride) * D + dc * 8;
-      if (t < L) x0 = load16(vp);
-      if (t + 1 < L) x1 = load16(vp + it.rstride * D);
-      const int pos = vt_pos(2 * kp);
-#pragma unroll
-      for (int i = 0; i < 8; ++i) {
-        const unsigned lo = (x0[i >> 1] >> (16 * (i & 1))) & 0xffffu;
-        const unsigned hv = (x1[i >> 1] >> (16 * (i & 1))) & 0xffffu;
-        *reinterpret_cast<unsigned*>(&sm.vt[(dc * 8 + i) * SmemBf16<D>::VSTR + pos]) =
-            lo | (hv << 16);
-      }
-    }
-    __syncthreads();
+    const int cur = jt & 1;
+    const int k0 = jt * BN;
+    const bool more = jt + 1 < ntile;
+    if (more) load_tile(jt + 1);
 
-    // S^T = K Q^T for two 32-key blocks.
-    f32x16 acc_s[2];
+    // Tiles entirely after this wave's queries are skipped (causal).
+    if (!(a.causal && k0 > wq_lo + 31)) {
+      // S^T = K Q^T, one 32x32 block per 32 keys.
+      f32x16 acc_s[SB];
 #pragma unroll
-    for (int kb = 0; kb < 2; ++kb) {
-      acc_s[kb] = f32x16{};
+      for (int kb = 0; kb < SB; ++kb) {
+        acc_s[kb] = f32x16{};
 #pragma unroll
-      for (int c = 0; c < KC; ++c) {
-        const u32x4 ka = *reinterpret_cast<const u32x4*>(
-            &sm.k[(kb * 32 + qr) * SmemBf16<D>::KSTR + 16 * c + 8 * hi]);
-        acc_s[kb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(__builtin_bit_cast(bf16x8, ka),
-                                                            qreg[c], acc_s[kb], 0, 0, 0);
-      }
-    }
-
-    // Mask keys after the query (causal) and keys past the segment's end.
-    const bool need_mask = (a.causal && k0 + kBN - 1 > wq_lo) || (k0 + kBN > L);
-    if (need_mask) {
-      const int lim = a.causal ? min(tq_row, L - 1) : L - 1;
-#pragma unroll
-      for (int kb = 0; kb < 2; ++kb)
-#pragma unroll
-        for (int j = 0; j < 16; ++j) {
-          const int key = k0 + kb * 32 + 8 * (j >> 2) + 4 * hi + (j & 3);
-          if (key > lim) acc_s[kb][j] = -INFINITY;
-        }
-    }
-
-    // Online softmax for this lane's query (exp2 domain, scale folded in).
-    float mx = acc_s[0][0];
-#pragma unroll
-    for (int kb = 0; kb < 2; ++kb)
-#pragma unroll
-      for (int j = 0; j < 16; ++j) mx = fmaxf(mx, acc_s[kb][j]);
-    mx = fmaxf(mx, __shfl_xor(mx, 32));
-    const float m_new = fmaxf(m_run, mx * a.scale_log2);
-    const float alpha = __builtin_amdgcn_exp2f(m_run - m_new);
-    m_run = m_new;
-    float psum = 0.0f;
-#pragma unroll
-    for (int kb = 0; kb < 2; ++kb)
-#pragma unroll
-      for (int j = 0; j < 16; ++j) {
-        const float p = __builtin_amdgcn_exp2f(fmaf(acc_s[kb][j], a.scale_log2, -m_new));
-        acc_s[kb][j] = p;
-        psum += p;
-      }
-    l_run = fmaf(l_run, alpha, psum);
-#pragma unroll
-    for (int db = 0; db < DB; ++db)
-#pragma unroll
-      for (int j = 0; j < 16; ++j) acc_o[db][j] *= alpha;
-
-    // O^T += V^T P^T, 16 keys per MFMA step.
-#pragma unroll
-    for (int kb = 0; kb < 2; ++kb)
-#pragma unroll
-      for (int kk = 0; kk < 2; ++kk) {
-        bf16x8 pb;
-#pragma unroll
-        for (int e = 0; e < 8; ++e) pb[e] = (__bf16)acc_s[kb][8 * kk + e];
-#pragma unroll
-        for (int db = 0; db < DB; ++db) {
-          const u32x4 va = *reinterpret_cast<const u32x4*>(
-              &sm.vt[(db * 32 + qr) * SmemBf16<D>::VSTR + (kb * 2 + kk) * 16 + 8 * hi]);
-          acc_o[db] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(__builtin_bit_cast(bf16x8, va),
-                                                              pb, acc_o[db], 0, 0, 0);
+        for (int c = 0; c < KC; ++c) {
+          const u32x4 ka = *reinterpret_cast<const u32x4*>(
+              &sm.k[cur][(kb * 32 + qr) * Smem::KSTR + 16 * c + 8 * hi]);
+          acc_s[kb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(__builtin_bit_cast(bf16x8, ka),
+                                                              qreg[c], acc_s[kb], 0, 0, 0);
         }
       }
+      // Mask keys after the query (causal) and past the segment's end.
+      if ((a.causal && k0 + BN - 1 > wq_lo) || k0 + BN > L) {
+        const int base = k0 + 4 * hi - lim;   // key - lim = base + offset(kb, j)
+#pragma unroll
+        for (int kb = 0; kb < SB; ++kb)
+#pragma unroll
+          for (int j = 0; j < 16; ++j)
+            if (base + kb * 32 + 8 * (j >> 2) + (j & 3) > 0) acc_s[kb][j] = -INFINITY;
+      }
+      // Tile max of this lane's query, across both half-waves.
+      float mx = -INFINITY;
+#pragma unroll
+      for (int kb = 0; kb < SB; ++kb)
+#pragma unroll
+        for (int j = 0; j < 16; j += 2) mx = fmaxf(mx, fmaxf(acc_s[kb][j], acc_s[kb][j + 1]));
+      mx = fmaxf(mx, __shfl_xor(mx, 32)) * a.scale_log2;
+      // Lazy rescale: move the reference max only when some row of the wave
+      // would otherwise see probabilities above 2^kRescaleSlack.
+      if (__any(mx > m_run + kRescaleSlack)) {
+        const float m_new = fmaxf(m_run, mx);
+        const float alpha = __builtin_amdgcn_exp2f(m_run - m_new);
+        m_run = m_new;
+        l_run *= alpha;
+#pragma unroll
+        for (int db = 0; db < DB; ++db)
+#pragma unroll
+          for (int j = 0; j < 16; ++j) acc_o[db][j] *= alpha;
+      }
+      // P = exp2(scale*log2e*S - m); bf16 P feeds the PV MFMA and the row sum.
+#pragma unroll
+      for (int kb = 0; kb < SB; ++kb)
+#pragma unroll
+        for (int kk = 0; kk < 2; ++kk) {
+          bf16x8 pb;
+#pragma unroll
+          for (int e = 0; e < 8; ++e)
+            pb[e] = (__bf16)__builtin_amdgcn_exp2f(fmaf(acc_s[kb][8 * kk + e], a.scale_log2, -m_run));
+#pragma unroll
+          for (int e = 0; e < 8; e += 2) {
+            bf16x2 pr = {pb[e], pb[e + 1]};
+            l_run = __builtin_amdgcn_fdot2_f32_bf16(pr, bf16x2{(__bf16)1.0f, (__bf16)1.0f}, l_run, false);
+          }
+#pragma unroll
+          for (int db = 0; db < DB; ++db) {
+            const u32x4 va = *reinterpret_cast<const u32x4*>(
+                &sm.vt[cur][(db * 32 + qr) * Smem::VSTR + (kb * 2 + kk) * 16 + 8 * hi]);
+            acc_o[db] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(__builtin_bit_cast(bf16x8, va),
+                                                                pb, acc_o[db], 0, 0, 0);
+          }
+        }
+    }
+    if (more) store_tile(cur ^ 1);
+    __syncthreads();
   }
 
   // Epilogue: normalise and write this lane's row of the per-pattern output.
@@ -393,15 +450,16 @@ hipError_t launch_attention(const Plan& plan, const void* q, const void* k, cons
       pa.nseg = static_cast<int32_t>(pp.nseg);
       pa.lmax = static_cast<int32_t>(pp.lmax);
       pa.ntiles = static_cast<int32_t>(pp.ntiles);
-      pa.item_begin = static_cast<int32_t>(pp.item_begin);
+      pa.units = static_cast<int32_t>(pp.units);
       pa.o_off = static_cast<int64_t>(pp.o_off / 4);
       pa.lse_off = static_cast<int64_t>(pp.lse_off / 4);
     } else {
-      pa = PatArgs{1, 1, 1, 1, 1, INT32_MAX, 0, 0};
+      pa = PatArgs{1, 1, 1, 1, 1, 0, 0, 0};
     }
   }
   if (plan.total_items == 0) return hipSuccess;
-  const dim3 grid(static_cast<unsigned>(plan.total_items));
+  // XCD 0 holds the most units of every pattern; the launch covers 8 times its slots.
+  const dim3 grid(static_cast<unsigned>(plan.launch_items));
   if (plan.dtype == DA_BF16) {
     switch (plan.D) {
       case 32: hipLaunchKernelGGL(attn_fwd_bf16<32>, grid, dim3(kThreads), 0, stream, a); break;

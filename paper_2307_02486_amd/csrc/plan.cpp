@@ -95,7 +95,11 @@ int make_plan(int64_t B, int64_t N, int64_t H, int64_t D, const da_pattern_t* pa
       pairs += (long double)B * heads * (nfull * pf + pt);
     }
   }
-  if (items >= (int64_t{1} << 31)) return DA_EINVAL;
+  int64_t launch = 0;
+  for (int i = 0; i < p.npat; ++i) launch += (p.pat[i].units + 7) / 8 * p.pat[i].ntiles;
+  launch *= 8;
+  if (items >= (int64_t{1} << 31) || launch >= (int64_t{1} << 31)) return DA_EINVAL;
+  p.launch_items = launch;
   // the combine stage launches one workgroup per 8..32 positions of each (b, h)
   if ((N + 7) / 8 * B * H >= (int64_t{1} << 31)) return DA_EINVAL;
   p.total_items = items;

@@ -54,6 +54,7 @@ struct Plan {
   int block_m;        // query rows per attention work item
   PatternPlan pat[DA_MAX_PATTERNS];
   int64_t total_items;
+  int64_t launch_items;  // workgroups of the attention launch (XCD-balanced, >= total_items)
   uint64_t workspace_bytes;
   int64_t covered_rows;
   double sparse_flops;
