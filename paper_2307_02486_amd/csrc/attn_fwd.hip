@@ -108,7 +108,15 @@ constexpr int kThreads = 256; // four waves
 constexpr float kRescaleSlack = 8.0f;
 
 // Keys per K/V tile for a head dim: 128 where the registers allow it.
-template <int D> struct KeyTile { static constexpr int value = D <= 64 ? 128 : 64; };
+#ifndef DA_KEY_TILE_SMALL_D
+#define DA_KEY_TILE_SMALL_D 64
+#endif
+// 32-key blocks of S^T whose K fragments are read from LDS together, before
+// their MFMAs, so LDS latency is paid once per group rather than per MFMA.
+#ifndef DA_QK_GROUP
+#define DA_QK_GROUP 2
+#endif
+template <int D> struct KeyTile { static constexpr int value = D <= 64 ? DA_KEY_TILE_SMALL_D : 64; };
 
 // Position of key `key` inside a transposed V row: within each group of 16
 // keys, keys {0-3, 8-11} come first and {4-7, 12-15} second, which is the
@@ -128,7 +136,20 @@ struct SmemBf16 {
 
 __device__ inline u32x4 load16(const u16* p) { return *reinterpret_cast<const u32x4*>(p); }
 
-template <int D>
+// The value held by lane l ^ 32 (the other half-wave), via v_permlane32_swap.
+__device__ inline float other_half(float x) {
+  const unsigned u = __builtin_bit_cast(unsigned, x);
+  const auto sw = __builtin_amdgcn_permlane32_swap(u, u, false, false);
+  const unsigned lane = __builtin_amdgcn_mbcnt_hi(~0u, __builtin_amdgcn_mbcnt_lo(~0u, 0u));
+  return __builtin_bit_cast(float, lane < 32 ? sw[1] : sw[0]);
+}
+
+// Word 3 of a raw buffer resource on gfx9-family GPUs (32-bit data format,
+// no swizzle); with stride 0 the size field is a byte count and reads at or
+// beyond it return zero.
+constexpr int kBufferFlags = 0x00020000;
+
+template <int D, bool kBufferLoads>
 __global__ __launch_bounds__(kThreads) void attn_fwd_bf16(AttnArgs a) {
   static_assert(D % 32 == 0, "head dim must be a multiple of 32");
   constexpr int BN = KeyTile<D>::value;
@@ -142,11 +163,11 @@ __global__ __launch_bounds__(kThreads) void attn_fwd_bf16(AttnArgs a) {
   __shared__ __attribute__((aligned(16))) Smem sm;
 
   Item it;
-  if (!decode_item(a, blockIdx.x, kBM, it)) return;
+  if (!decode_item(a, __builtin_amdgcn_workgroup_id_x(), kBM, it)) return;
   const PatArgs& P = a.pat[it.pi];
   const u16* __restrict__ qg = static_cast<const u16*>(a.q);
 
-  const int tid = threadIdx.x;
+  const int tid = __builtin_amdgcn_workitem_id_x();
   const int lane = tid & 63;
   const int wv = tid >> 6;
   const int qr = lane & 31;   // query column of this lane in S^T / O^T
@@ -169,40 +190,64 @@ __global__ __launch_bounds__(kThreads) void attn_fwd_bf16(AttnArgs a) {
     }
   }
 
-  // Fixed per-thread roles in the tile loads; pointers advance by BN kept rows
-  // per tile.
+  // Fixed per-thread roles in the tile loads:
   //  K chunk i: key (tid + 256i) / (D/8), head-dim chunk (tid + 256i) % (D/8)
   //  V task i:  keys 2kp, 2kp+1 with kp = (tid + 256i) % (BN/2), chunk (tid + 256i) / (BN/2)
-  const u16* kp_[KT];
-  int kkey[KT];
+  // With kBufferLoads, a tile is read through a buffer resource whose base is
+  // the tile's first kept row and whose size ends at the segment's last kept
+  // row: each thread keeps a fixed 32-bit offset, and rows past the end read
+  // as zero without any per-load test.  Otherwise 64-bit pointers and tests.
+  int kkey[KT], kdc[KT];
 #pragma unroll
   for (int i = 0; i < KT; ++i) {
     const int task = tid + i * kThreads;
     kkey[i] = task / (D / 8);
-    kp_[i] = static_cast<const u16*>(a.k) + it.row0 * D + (int64_t)kkey[i] * row_step + (task % (D / 8)) * 8;
+    kdc[i] = task % (D / 8);
   }
-  const u16* vp_[VT];
-  int vkey[VT];
+  int vkey[VT], vdc[VT];
 #pragma unroll
   for (int i = 0; i < VT; ++i) {
     const int task = min(tid + i * kThreads, VTASKS - 1);
     vkey[i] = 2 * (task % (BN / 2));
-    vp_[i] = static_cast<const u16*>(a.v) + it.row0 * D + (int64_t)vkey[i] * row_step + (task / (BN / 2)) * 8;
+    vdc[i] = task / (BN / 2);
   }
+  const u16* kbase = static_cast<const u16*>(a.k) + it.row0 * D;
+  const u16* vbase = static_cast<const u16*>(a.v) + it.row0 * D;
   const int64_t tile_step = row_step * BN;
 
   u32x4 rk[KT], rv0[VT], rv1[VT];
   auto load_tile = [&](int jt) {
     const int k0 = jt * BN;
-    const int64_t off = tile_step * jt;
+    if constexpr (kBufferLoads) {
+      const uint64_t row_bytes = static_cast<uint64_t>(row_step) * 2;
+      const uint64_t valid = static_cast<uint64_t>(L - k0) * row_bytes;
+      const int nrec = static_cast<int>(valid < 0x7fffffffull ? valid : 0x7fffffffull);
+      const __amdgpu_buffer_rsrc_t rk_src = __builtin_amdgcn_make_buffer_rsrc(
+          const_cast<u16*>(kbase + tile_step * jt), 0, nrec, kBufferFlags);
+      const __amdgpu_buffer_rsrc_t rv_src = __builtin_amdgcn_make_buffer_rsrc(
+          const_cast<u16*>(vbase + tile_step * jt), 0, nrec, kBufferFlags);
 #pragma unroll
-    for (int i = 0; i < KT; ++i)
-      rk[i] = k0 + kkey[i] < L ? load16(kp_[i] + off) : u32x4{0, 0, 0, 0};
+      for (int i = 0; i < KT; ++i)
+        rk[i] = __builtin_amdgcn_raw_buffer_load_b128(
+            rk_src, static_cast<int>(kkey[i] * row_bytes) + kdc[i] * 16, 0, 0);
 #pragma unroll
-    for (int i = 0; i < VT; ++i) {
-      const int t = k0 + vkey[i];
-      rv0[i] = t < L ? load16(vp_[i] + off) : u32x4{0, 0, 0, 0};
-      rv1[i] = t + 1 < L ? load16(vp_[i] + off + row_step) : u32x4{0, 0, 0, 0};
+      for (int i = 0; i < VT; ++i) {
+        const int off = static_cast<int>(vkey[i] * row_bytes) + vdc[i] * 16;
+        rv0[i] = __builtin_amdgcn_raw_buffer_load_b128(rv_src, off, 0, 0);
+        rv1[i] = __builtin_amdgcn_raw_buffer_load_b128(rv_src, off + static_cast<int>(row_bytes), 0, 0);
+      }
+    } else {
+      const int64_t off = tile_step * jt;
+#pragma unroll
+      for (int i = 0; i < KT; ++i)
+        rk[i] = k0 + kkey[i] < L ? load16(kbase + off + kkey[i] * row_step + kdc[i] * 8) : u32x4{0, 0, 0, 0};
+#pragma unroll
+      for (int i = 0; i < VT; ++i) {
+        const int t = k0 + vkey[i];
+        const u16* vp = vbase + off + vkey[i] * row_step + vdc[i] * 8;
+        rv0[i] = t < L ? load16(vp) : u32x4{0, 0, 0, 0};
+        rv1[i] = t + 1 < L ? load16(vp + row_step) : u32x4{0, 0, 0, 0};
+      }
     }
   };
   auto store_tile = [&](int buf) {
@@ -249,17 +294,27 @@ __global__ __launch_bounds__(kThreads) void attn_fwd_bf16(AttnArgs a) {
 
     // Tiles entirely after this wave's queries are skipped (causal).
     if (!(a.causal && k0 > wq_lo + 31)) {
-      // S^T = K Q^T, one 32x32 block per 32 keys.
+      // S^T = K Q^T, one 32x32 block per 32 keys; the K fragments of a group
+      // of blocks are all requested from LDS before the group's MFMAs.
       f32x16 acc_s[SB];
+      constexpr int QG = DA_QK_GROUP < SB ? DA_QK_GROUP : SB;
 #pragma unroll
-      for (int kb = 0; kb < SB; ++kb) {
-        acc_s[kb] = f32x16{};
+      for (int kb0 = 0; kb0 < SB; kb0 += QG) {
+        u32x4 kf[QG][KC];
 #pragma unroll
-        for (int c = 0; c < KC; ++c) {
-          const u32x4 ka = *reinterpret_cast<const u32x4*>(
-              &sm.k[cur][(kb * 32 + qr) * Smem::KSTR + 16 * c + 8 * hi]);
-          acc_s[kb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(__builtin_bit_cast(bf16x8, ka),
-                                                              qreg[c], acc_s[kb], 0, 0, 0);
+        for (int g = 0; g < QG; ++g)
+#pragma unroll
+          for (int c = 0; c < KC; ++c)
+            kf[g][c] = *reinterpret_cast<const u32x4*>(
+                &sm.k[cur][((kb0 + g) * 32 + qr) * Smem::KSTR + 16 * c + 8 * hi]);
+        __builtin_amdgcn_sched_barrier(0);  // keep the reads ahead of the MFMAs
+#pragma unroll
+        for (int g = 0; g < QG; ++g) {
+          acc_s[kb0 + g] = f32x16{};
+#pragma unroll
+          for (int c = 0; c < KC; ++c)
+            acc_s[kb0 + g] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(
+                __builtin_bit_cast(bf16x8, kf[g][c]), qreg[c], acc_s[kb0 + g], 0, 0, 0);
         }
       }
       // Mask keys after the query (causal) and past the segment's end.
@@ -277,7 +332,7 @@ __global__ __launch_bounds__(kThreads) void attn_fwd_bf16(AttnArgs a) {
       for (int kb = 0; kb < SB; ++kb)
 #pragma unroll
         for (int j = 0; j < 16; j += 2) mx = fmaxf(mx, fmaxf(acc_s[kb][j], acc_s[kb][j + 1]));
-      mx = fmaxf(mx, __shfl_xor(mx, 32)) * a.scale_log2;
+      mx = fmaxf(mx, other_half(mx)) * a.scale_log2;
       // Lazy rescale: move the reference max only when some row of the wave
       // would otherwise see probabilities above 2^kRescaleSlack.
       if (__any(mx > m_run + kRescaleSlack)) {
@@ -291,8 +346,17 @@ __global__ __launch_bounds__(kThreads) void attn_fwd_bf16(AttnArgs a) {
           for (int j = 0; j < 16; ++j) acc_o[db][j] *= alpha;
       }
       // P = exp2(scale*log2e*S - m); bf16 P feeds the PV MFMA and the row sum.
+      // The V^T fragments of a 32-key block are requested before its exps.
 #pragma unroll
-      for (int kb = 0; kb < SB; ++kb)
+      for (int kb = 0; kb < SB; ++kb) {
+        u32x4 vf[2][DB];
+#pragma unroll
+        for (int kk = 0; kk < 2; ++kk)
+#pragma unroll
+          for (int db = 0; db < DB; ++db)
+            vf[kk][db] = *reinterpret_cast<const u32x4*>(
+                &sm.vt[cur][(db * 32 + qr) * Smem::VSTR + (kb * 2 + kk) * 16 + 8 * hi]);
+        __builtin_amdgcn_sched_barrier(0);  // keep the reads ahead of the exps
 #pragma unroll
         for (int kk = 0; kk < 2; ++kk) {
           bf16x8 pb;
@@ -305,20 +369,18 @@ __global__ __launch_bounds__(kThreads) void attn_fwd_bf16(AttnArgs a) {
             l_run = __builtin_amdgcn_fdot2_f32_bf16(pr, bf16x2{(__bf16)1.0f, (__bf16)1.0f}, l_run, false);
           }
 #pragma unroll
-          for (int db = 0; db < DB; ++db) {
-            const u32x4 va = *reinterpret_cast<const u32x4*>(
-                &sm.vt[cur][(db * 32 + qr) * Smem::VSTR + (kb * 2 + kk) * 16 + 8 * hi]);
-            acc_o[db] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(__builtin_bit_cast(bf16x8, va),
+          for (int db = 0; db < DB; ++db)
+            acc_o[db] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(__builtin_bit_cast(bf16x8, vf[kk][db]),
                                                                 pb, acc_o[db], 0, 0, 0);
-          }
         }
+      }
     }
     if (more) store_tile(cur ^ 1);
     __syncthreads();
   }
 
   // Epilogue: normalise and write this lane's row of the per-pattern output.
-  const float l_tot = l_run + __shfl_xor(l_run, 32);
+  const float l_tot = l_run + other_half(l_run);
   if (!q_valid) return;
   const float inv = 1.0f / l_tot;
   const int64_t wrow = (int64_t)it.unit * P.lmax + tq_row;
@@ -346,12 +408,12 @@ __global__ __launch_bounds__(kBM32) void attn_fwd_f32(AttnArgs a) {
   __shared__ __attribute__((aligned(16))) float ks[kBN32][D];
   __shared__ __attribute__((aligned(16))) float vs[kBN32][D];
   Item it;
-  if (!decode_item(a, blockIdx.x, kBM32, it)) return;
+  if (!decode_item(a, __builtin_amdgcn_workgroup_id_x(), kBM32, it)) return;
   const PatArgs& P = a.pat[it.pi];
   const float* __restrict__ qg = static_cast<const float*>(a.q);
   const float* __restrict__ kg = static_cast<const float*>(a.k);
   const float* __restrict__ vg = static_cast<const float*>(a.v);
-  const int tid = threadIdx.x;
+  const int tid = __builtin_amdgcn_workitem_id_x();
   const int L = it.L;
   const int q0 = it.tq * kBM32;
   const int qend = min(q0 + kBM32, L);
@@ -462,9 +524,18 @@ hipError_t launch_attention(const Plan& plan, const void* q, const void* k, cons
   const dim3 grid(static_cast<unsigned>(plan.launch_items));
   if (plan.dtype == DA_BF16) {
     switch (plan.D) {
-      case 32: hipLaunchKernelGGL(attn_fwd_bf16<32>, grid, dim3(kThreads), 0, stream, a); break;
-      case 64: hipLaunchKernelGGL(attn_fwd_bf16<64>, grid, dim3(kThreads), 0, stream, a); break;
-      case 128: hipLaunchKernelGGL(attn_fwd_bf16<128>, grid, dim3(kThreads), 0, stream, a); break;
+      case 32:
+        if (plan.offsets32) hipLaunchKernelGGL((attn_fwd_bf16<32, true>), grid, dim3(kThreads), 0, stream, a);
+        else hipLaunchKernelGGL((attn_fwd_bf16<32, false>), grid, dim3(kThreads), 0, stream, a);
+        break;
+      case 64:
+        if (plan.offsets32) hipLaunchKernelGGL((attn_fwd_bf16<64, true>), grid, dim3(kThreads), 0, stream, a);
+        else hipLaunchKernelGGL((attn_fwd_bf16<64, false>), grid, dim3(kThreads), 0, stream, a);
+        break;
+      case 128:
+        if (plan.offsets32) hipLaunchKernelGGL((attn_fwd_bf16<128, true>), grid, dim3(kThreads), 0, stream, a);
+        else hipLaunchKernelGGL((attn_fwd_bf16<128, false>), grid, dim3(kThreads), 0, stream, a);
+        break;
       default: return hipErrorInvalidValue;
     }
   } else {

@@ -100,6 +100,12 @@ int make_plan(int64_t B, int64_t N, int64_t H, int64_t D, const da_pattern_t* pa
   launch *= 8;
   if (items >= (int64_t{1} << 31) || launch >= (int64_t{1} << 31)) return DA_EINVAL;
   p.launch_items = launch;
+  // A key tile of the attention kernel spans at most 128 kept rows, each r*H*D
+  // elements after the previous one; 32-bit byte offsets inside a tile (plus
+  // one row) must stay below 2^31.
+  p.offsets32 = true;
+  for (int i = 0; i < p.npat; ++i)
+    if (static_cast<double>(p.pat[i].r) * H * D * esize * 129.0 >= 2147483648.0) p.offsets32 = false;
   // the combine stage launches one workgroup per 8..32 positions of each (b, h)
   if ((N + 7) / 8 * B * H >= (int64_t{1} << 31)) return DA_EINVAL;
   p.total_items = items;

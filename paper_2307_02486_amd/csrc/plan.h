@@ -55,6 +55,7 @@ struct Plan {
   PatternPlan pat[DA_MAX_PATTERNS];
   int64_t total_items;
   int64_t launch_items;  // workgroups of the attention launch (XCD-balanced, >= total_items)
+  bool offsets32;        // every key tile spans < 2^31 bytes: 32-bit buffer offsets suffice
   uint64_t workspace_bytes;
   int64_t covered_rows;
   double sparse_flops;

@@ -76,6 +76,8 @@ EDGE = [
     (1, 160, 2, 32, "f32", [(160, 1)], True),
     (1, 4096, 2, 128, "bf16", [(4096, 1), (2048, 2)], True),
     (1, 64, 16, 64, "bf16", [(64, 64), (64, 1)], True),   # r = w
+    # r*H*D so large that a key tile spans >= 2 GiB of rows: 64-bit addressing path
+    (1, 1024, 64, 128, "bf16", [(1024, 1), (1024, 1024)], True),
 ]
 
 
