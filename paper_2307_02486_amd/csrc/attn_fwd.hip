@@ -100,8 +100,11 @@ __device__ inline bool decode_item(const AttnArgs& a, int bid, int block_m, Item
 // ---------------------------------------------------------------------------
 // bf16 MFMA kernel
 // ---------------------------------------------------------------------------
-constexpr int kBM = 128;      // query rows per work item
-constexpr int kThreads = 256; // four waves
+#ifndef DA_BF16_WAVES
+#define DA_BF16_WAVES 4
+#endif
+constexpr int kThreads = 64 * DA_BF16_WAVES;  // waves of 32 query rows each
+constexpr int kBM = 32 * DA_BF16_WAVES;       // query rows per work item
 // A row's running max is raised only when a tile's max exceeds it by more than
 // this (log2 units); until then probabilities may reach 2^kRescaleSlack, which
 // bf16 and the fp32 sums hold exactly as well as values below 1.
@@ -115,6 +118,11 @@ constexpr float kRescaleSlack = 8.0f;
 // their MFMAs, so LDS latency is paid once per group rather than per MFMA.
 #ifndef DA_QK_GROUP
 #define DA_QK_GROUP 2
+#endif
+// Scores from q pre-multiplied by scale*log2(e) and rounded to bf16 (1), or
+// from q as given with the scale applied per score in fp32 (0).
+#ifndef DA_PRESCALED_Q
+#define DA_PRESCALED_Q 1
 #endif
 template <int D> struct KeyTile { static constexpr int value = D <= 64 ? DA_KEY_TILE_SMALL_D : 64; };
 
@@ -156,7 +164,8 @@ __global__ __launch_bounds__(kThreads) void attn_fwd_bf16(AttnArgs a) {
   constexpr int KC = D / 16;  // MFMA k-steps over the head dim
   constexpr int DB = D / 32;  // 32-wide blocks of the head dim in O^T
   constexpr int SB = BN / 32; // 32-key blocks of S^T per tile
-  constexpr int KT = BN * D / 8 / kThreads;                 // 16-B K chunks per thread per tile
+  constexpr int KTASKS = BN * D / 8;                        // 16-B K chunks per tile
+  constexpr int KT = (KTASKS + kThreads - 1) / kThreads;    // K chunks per thread
   constexpr int VTASKS = (BN / 2) * (D / 8);                // (key pair, 8-wide chunk) V tasks
   constexpr int VT = (VTASKS + kThreads - 1) / kThreads;    // V tasks per thread
   using Smem = SmemBf16<D, BN>;
@@ -186,7 +195,17 @@ __global__ __launch_bounds__(kThreads) void attn_fwd_bf16(AttnArgs a) {
 #pragma unroll
     for (int c = 0; c < KC; ++c) {
       u32x4 x = q_valid ? load16(qp + 16 * c) : u32x4{0, 0, 0, 0};
+#if DA_PRESCALED_Q
+      // q * scale * log2(e), rounded to bf16: the MFMA then yields scores in
+      // log2 units and the exponent needs no per-score multiply.
+#pragma unroll
+      for (int e = 0; e < 8; ++e) {
+        const unsigned bits = (x[e >> 1] >> (16 * (e & 1))) << 16;
+        qreg[c][e] = (__bf16)(__builtin_bit_cast(float, bits) * a.scale_log2);
+      }
+#else
       qreg[c] = __builtin_bit_cast(bf16x8, x);
+#endif
     }
   }
 
@@ -200,7 +219,7 @@ __global__ __launch_bounds__(kThreads) void attn_fwd_bf16(AttnArgs a) {
   int kkey[KT], kdc[KT];
 #pragma unroll
   for (int i = 0; i < KT; ++i) {
-    const int task = tid + i * kThreads;
+    const int task = min(tid + i * kThreads, KTASKS - 1);
     kkey[i] = task / (D / 8);
     kdc[i] = task % (D / 8);
   }
@@ -254,7 +273,8 @@ __global__ __launch_bounds__(kThreads) void attn_fwd_bf16(AttnArgs a) {
 #pragma unroll
     for (int i = 0; i < KT; ++i) {
       const int task = tid + i * kThreads;
-      *reinterpret_cast<u32x4*>(&sm.k[buf][(task / (D / 8)) * Smem::KSTR + (task % (D / 8)) * 8]) = rk[i];
+      if (KTASKS % kThreads == 0 || task < KTASKS)
+        *reinterpret_cast<u32x4*>(&sm.k[buf][(task / (D / 8)) * Smem::KSTR + (task % (D / 8)) * 8]) = rk[i];
     }
 #pragma unroll
     for (int i = 0; i < VT; ++i) {
@@ -275,7 +295,12 @@ __global__ __launch_bounds__(kThreads) void attn_fwd_bf16(AttnArgs a) {
   f32x16 acc_o[DB];
 #pragma unroll
   for (int db = 0; db < DB; ++db) acc_o[db] = f32x16{};
+#if DA_PRESCALED_Q
+  float m_run = 0.0f;     // reference max of scaled scores (log2 domain), set by tile 0
+  f32x16 negm = f32x16{}; // -m_run in every slot: the initial value of each S' block
+#else
   float m_run = kNegBig;  // reference max of scaled scores (log2 domain)
+#endif
   float l_run = 0.0f;     // this half-wave's share of the running denominator
 
   const int kv_end = a.causal ? qend : L;
@@ -308,14 +333,24 @@ __global__ __launch_bounds__(kThreads) void attn_fwd_bf16(AttnArgs a) {
             kf[g][c] = *reinterpret_cast<const u32x4*>(
                 &sm.k[cur][((kb0 + g) * 32 + qr) * Smem::KSTR + 16 * c + 8 * hi]);
         __builtin_amdgcn_sched_barrier(0);  // keep the reads ahead of the MFMAs
+#ifdef DA_SETPRIO
+        __builtin_amdgcn_s_setprio(1);
+#endif
 #pragma unroll
         for (int g = 0; g < QG; ++g) {
+#if DA_PRESCALED_Q
+          acc_s[kb0 + g] = negm;  // scores start at -m: S' = q'k - m
+#else
           acc_s[kb0 + g] = f32x16{};
+#endif
 #pragma unroll
           for (int c = 0; c < KC; ++c)
             acc_s[kb0 + g] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(
                 __builtin_bit_cast(bf16x8, kf[g][c]), qreg[c], acc_s[kb0 + g], 0, 0, 0);
         }
+#ifdef DA_SETPRIO
+        __builtin_amdgcn_s_setprio(0);
+#endif
       }
       // Mask keys after the query (causal) and past the segment's end.
       if ((a.causal && k0 + BN - 1 > wq_lo) || k0 + BN > L) {
@@ -332,6 +367,28 @@ __global__ __launch_bounds__(kThreads) void attn_fwd_bf16(AttnArgs a) {
       for (int kb = 0; kb < SB; ++kb)
 #pragma unroll
         for (int j = 0; j < 16; j += 2) mx = fmaxf(mx, fmaxf(acc_s[kb][j], acc_s[kb][j + 1]));
+#if DA_PRESCALED_Q
+      mx = fmaxf(mx, other_half(mx));  // already relative to m_run, log2 units
+      // Lazy rescale: the first tile fixes the reference max; later tiles move
+      // it only when some row of the wave would see probabilities above
+      // 2^kRescaleSlack.
+      if (jt == 0 || __any(mx > kRescaleSlack)) {
+        const float delta = jt == 0 ? mx : fmaxf(mx, 0.0f);
+        const float alpha = __builtin_amdgcn_exp2f(-delta);
+        m_run += delta;
+        l_run *= alpha;
+#pragma unroll
+        for (int db = 0; db < DB; ++db)
+#pragma unroll
+          for (int j = 0; j < 16; ++j) acc_o[db][j] *= alpha;
+#pragma unroll
+        for (int kb = 0; kb < SB; ++kb)
+#pragma unroll
+          for (int j = 0; j < 16; ++j) acc_s[kb][j] -= delta;
+#pragma unroll
+        for (int j = 0; j < 16; ++j) negm[j] = -m_run;
+      }
+#else
       mx = fmaxf(mx, other_half(mx)) * a.scale_log2;
       // Lazy rescale: move the reference max only when some row of the wave
       // would otherwise see probabilities above 2^kRescaleSlack.
@@ -345,6 +402,7 @@ __global__ __launch_bounds__(kThreads) void attn_fwd_bf16(AttnArgs a) {
 #pragma unroll
           for (int j = 0; j < 16; ++j) acc_o[db][j] *= alpha;
       }
+#endif
       // P = exp2(scale*log2e*S - m); bf16 P feeds the PV MFMA and the row sum.
       // The V^T fragments of a 32-key block are requested before its exps.
 #pragma unroll
@@ -362,7 +420,11 @@ __global__ __launch_bounds__(kThreads) void attn_fwd_bf16(AttnArgs a) {
           bf16x8 pb;
 #pragma unroll
           for (int e = 0; e < 8; ++e)
+#if DA_PRESCALED_Q
+            pb[e] = (__bf16)__builtin_amdgcn_exp2f(acc_s[kb][8 * kk + e]);
+#else
             pb[e] = (__bf16)__builtin_amdgcn_exp2f(fmaf(acc_s[kb][8 * kk + e], a.scale_log2, -m_run));
+#endif
 #pragma unroll
           for (int e = 0; e < 8; e += 2) {
             bf16x2 pr = {pb[e], pb[e + 1]};

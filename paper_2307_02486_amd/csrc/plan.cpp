@@ -17,7 +17,10 @@ FastDiv make_fastdiv(uint32_t d) {
   return f;
 }
 
-int block_m_for(int dtype) { return dtype == DA_BF16 ? 128 : 64; }
+#ifndef DA_BF16_WAVES
+#define DA_BF16_WAVES 4
+#endif
+int block_m_for(int dtype) { return dtype == DA_BF16 ? 32 * DA_BF16_WAVES : 64; }
 
 namespace {
 
