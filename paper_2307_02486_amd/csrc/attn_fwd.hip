@@ -26,6 +26,7 @@ typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
 typedef __bf16 bf16x2 __attribute__((ext_vector_type(2)));
 typedef float f32x16 __attribute__((ext_vector_type(16)));
 typedef float f32x4 __attribute__((ext_vector_type(4)));
+typedef _Float16 f16x4 __attribute__((ext_vector_type(4)));
 typedef unsigned int u32x4 __attribute__((ext_vector_type(4)));
 typedef unsigned short u16;
 
@@ -35,15 +36,15 @@ constexpr float kNegBig = -1.0e30f;   // finite "minus infinity" for running max
 
 struct PatArgs {
   int32_t w, r, nseg, lmax, ntiles, units;
-  int64_t o_off;    // float offset of this pattern's output rows in the workspace
-  int64_t lse_off;  // float offset of this pattern's lse in the workspace
+  int64_t o_off;    // byte offset of this pattern's output rows in the workspace
+  int64_t lse_off;  // byte offset of this pattern's lse in the workspace
 };
 
 struct AttnArgs {
   const void* q;
   const void* k;
   const void* v;
-  float* ws;
+  char* ws;
   int32_t B, N, H, npat, causal, total_items;
   float scale_log2;  // softmax scale times log2(e): scores go to exp2 directly
   PatArgs pat[DA_MAX_PATTERNS];
@@ -446,17 +447,18 @@ __global__ __launch_bounds__(kThreads) void attn_fwd_bf16(AttnArgs a) {
   if (!q_valid) return;
   const float inv = 1.0f / l_tot;
   const int64_t wrow = (int64_t)it.unit * P.lmax + tq_row;
-  float* orow = a.ws + P.o_off + wrow * D;
+  _Float16* orow = reinterpret_cast<_Float16*>(a.ws + P.o_off) + wrow * D;
 #pragma unroll
   for (int db = 0; db < DB; ++db)
 #pragma unroll
     for (int jj = 0; jj < 4; ++jj) {
-      f32x4 o;
+      f16x4 o;
 #pragma unroll
-      for (int e = 0; e < 4; ++e) o[e] = acc_o[db][4 * jj + e] * inv;
-      *reinterpret_cast<f32x4*>(orow + db * 32 + 8 * jj + 4 * hi) = o;
+      for (int e = 0; e < 4; ++e) o[e] = (_Float16)(acc_o[db][4 * jj + e] * inv);
+      *reinterpret_cast<f16x4*>(orow + db * 32 + 8 * jj + 4 * hi) = o;
     }
-  if (hi == 0) a.ws[P.lse_off + wrow] = (m_run + __builtin_amdgcn_logf(l_tot)) * kLn2;
+  if (hi == 0)
+    reinterpret_cast<float*>(a.ws + P.lse_off)[wrow] = (m_run + __builtin_amdgcn_logf(l_tot)) * kLn2;
 }
 
 // ---------------------------------------------------------------------------
@@ -542,11 +544,11 @@ __global__ __launch_bounds__(kBM32) void attn_fwd_f32(AttnArgs a) {
   if (!valid) return;
   const float inv = 1.0f / l_run;
   const int64_t wrow = (int64_t)it.unit * P.lmax + t;
-  float* orow = a.ws + P.o_off + wrow * D;
+  float* orow = reinterpret_cast<float*>(a.ws + P.o_off) + wrow * D;
 #pragma unroll
   for (int d = 0; d < D; d += 4)
     *reinterpret_cast<f32x4*>(orow + d) = f32x4{o[d] * inv, o[d + 1] * inv, o[d + 2] * inv, o[d + 3] * inv};
-  a.ws[P.lse_off + wrow] = (m_run + __builtin_amdgcn_logf(l_run)) * kLn2;
+  reinterpret_cast<float*>(a.ws + P.lse_off)[wrow] = (m_run + __builtin_amdgcn_logf(l_run)) * kLn2;
 }
 
 }  // namespace
@@ -557,7 +559,7 @@ hipError_t launch_attention(const Plan& plan, const void* q, const void* k, cons
   a.q = q;
   a.k = k;
   a.v = v;
-  a.ws = static_cast<float*>(workspace);
+  a.ws = static_cast<char*>(workspace);
   a.B = static_cast<int32_t>(plan.B);
   a.N = static_cast<int32_t>(plan.N);
   a.H = static_cast<int32_t>(plan.H);
@@ -575,8 +577,8 @@ hipError_t launch_attention(const Plan& plan, const void* q, const void* k, cons
       pa.lmax = static_cast<int32_t>(pp.lmax);
       pa.ntiles = static_cast<int32_t>(pp.ntiles);
       pa.units = static_cast<int32_t>(pp.units);
-      pa.o_off = static_cast<int64_t>(pp.o_off / 4);
-      pa.lse_off = static_cast<int64_t>(pp.lse_off / 4);
+      pa.o_off = static_cast<int64_t>(pp.o_off);
+      pa.lse_off = static_cast<int64_t>(pp.lse_off);
     } else {
       pa = PatArgs{1, 1, 1, 1, 1, 0, 0, 0};
     }

@@ -5,13 +5,14 @@
 // i's softmax denominator (Sec. 2.2, Eqs. 9-10).  It writes out [B,N,H,D] in
 // the input dtype and the combined lse [B,H,N] = log(sum_i s_i) in float32.
 //
-// A workgroup handles a run of consecutive positions p of one (b, h): each
-// lane owns four consecutive head-dim elements of one row, so a row of the
-// compact per-pattern output is read with D/4 16-byte loads and consecutive
-// positions of a dense pattern are consecutive in memory.  Whether pattern i
-// keeps row p for head h, and at which compact index t, follows from
-// g = p div w, t = (p - g w) div r and (p - g w) mod r == h mod r, with the
-// divisions done by multiply-shift constants prepared on the host.
+// A workgroup handles a run of consecutive positions p of one (b, h); each
+// lane owns eight consecutive head-dim elements of one row, so a row of a
+// per-pattern output is read with D/8 16-byte (fp16) or 32-byte (fp32) loads
+// and consecutive positions of a dense pattern are consecutive in memory.
+// Whether pattern i keeps row p for head h, and at which compact index t,
+// follows from g = p div w, t = (p - g w) div r and (p - g w) mod r ==
+// h mod r, with the divisions done by multiply-shift constants prepared on
+// the host.  All loads of a row are issued before any is consumed.
 #include <hip/hip_runtime.h>
 
 #include "kernels.h"
@@ -20,21 +21,24 @@ namespace da {
 namespace {
 
 typedef float f32x4 __attribute__((ext_vector_type(4)));
+typedef float f32x8 __attribute__((ext_vector_type(8)));
+typedef _Float16 f16x8 __attribute__((ext_vector_type(8)));
+typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
 
 constexpr float kLog2e = 1.442695040888963407f;
 constexpr float kLn2 = 0.693147180559945309f;
 constexpr int kThreads = 256;
 
 struct CombPat {
-  FastDiv fw;      // division by w
-  FastDiv fr;      // division by r
+  FastDiv fw;       // division by w
+  FastDiv fr;       // division by r
   int32_t nseg, lmax;
-  int64_t o_off;   // float offset of the pattern's output rows
-  int64_t lse_off; // float offset of the pattern's lse
+  int64_t o_off;    // byte offset of the pattern's output rows
+  int64_t lse_off;  // byte offset of the pattern's lse
 };
 
 struct CombArgs {
-  const float* ws;
+  const char* ws;
   void* out;
   float* lse;
   int32_t N, H, npat;
@@ -42,33 +46,55 @@ struct CombArgs {
   CombPat pat[DA_MAX_PATTERNS];
 };
 
-__device__ inline void store4(float* p, const f32x4& v) { *reinterpret_cast<f32x4*>(p) = v; }
+// Eight consecutive workspace elements as loaded (converted to fp32 when used).
+template <typename WsT> struct Vec8;
+template <> struct Vec8<_Float16> { typedef f16x8 type; };
+template <> struct Vec8<float> { typedef f32x8 type; };
 
-__device__ inline void store4(unsigned short* p, const f32x4& v) {
-  typedef __bf16 bf16x4 __attribute__((ext_vector_type(4)));
-  bf16x4 b;
-  b[0] = (__bf16)v[0];
-  b[1] = (__bf16)v[1];
-  b[2] = (__bf16)v[2];
-  b[3] = (__bf16)v[3];
-  *reinterpret_cast<bf16x4*>(p) = b;
+template <typename WsT>
+__device__ inline typename Vec8<WsT>::type load8(const WsT* p) {
+  return *reinterpret_cast<const typename Vec8<WsT>::type*>(p);
 }
 
-template <int D, typename OutT>
+__device__ inline f32x8 to_f32(const f16x8& h) {
+  f32x8 r;
+#pragma unroll
+  for (int e = 0; e < 8; ++e) r[e] = static_cast<float>(h[e]);
+  return r;
+}
+__device__ inline f32x8 to_f32(const f32x8& v) { return v; }
+
+__device__ inline void store8(float* p, const f32x8& v) {
+  *reinterpret_cast<f32x4*>(p) = f32x4{v[0], v[1], v[2], v[3]};
+  *reinterpret_cast<f32x4*>(p + 4) = f32x4{v[4], v[5], v[6], v[7]};
+}
+
+__device__ inline void store8(unsigned short* p, const f32x8& v) {
+  bf16x8 b;
+#pragma unroll
+  for (int e = 0; e < 8; ++e) b[e] = (__bf16)v[e];
+  *reinterpret_cast<bf16x8*>(p) = b;
+}
+
+template <int D, typename OutT, typename WsT>
 __global__ __launch_bounds__(kThreads) void combine_fwd(CombArgs a) {
-  constexpr int LPR = D / 4;             // lanes per row
-  constexpr int RPB = kThreads / LPR;    // rows per workgroup
-  const int tid = threadIdx.x;
-  const int bh = blockIdx.x / a.chunks;
-  const int p = (blockIdx.x - bh * a.chunks) * RPB + tid / LPR;
-  const int d0 = (tid % LPR) * 4;
+  constexpr int LPR = D / 8;            // lanes per row
+  constexpr int RPB = kThreads / LPR;   // rows per workgroup
+  const int tid = __builtin_amdgcn_workitem_id_x();
+  const int blk = __builtin_amdgcn_workgroup_id_x();
+  const int bh = blk / a.chunks;
+  const int p = (blk - bh * a.chunks) * RPB + tid / LPR;
+  const int d0 = (tid % LPR) * 8;
   if (p >= a.N) return;
   const int h = bh % a.H;
 
-  float m = -INFINITY;  // running max of lse_i (natural log)
-  float den = 0.0f;     // sum_i exp(lse_i - m)
-  f32x4 acc = f32x4{0, 0, 0, 0};
-  for (int i = 0; i < a.npat; ++i) {
+  // Issue the loads of every pattern that keeps this row.
+  typename Vec8<WsT>::type o[DA_MAX_PATTERNS];
+  float li[DA_MAX_PATTERNS];
+#pragma unroll
+  for (int i = 0; i < DA_MAX_PATTERNS; ++i) {
+    li[i] = -INFINITY;
+    if (i >= a.npat) continue;
     const CombPat& P = a.pat[i];
     const uint32_t g = P.fw.div(static_cast<uint32_t>(p));
     const uint32_t pos = static_cast<uint32_t>(p) - g * P.fw.d;
@@ -76,30 +102,36 @@ __global__ __launch_bounds__(kThreads) void combine_fwd(CombArgs a) {
     const uint32_t s = static_cast<uint32_t>(h) - P.fr.div(static_cast<uint32_t>(h)) * P.fr.d;
     if (pos - t * P.fr.d != s) continue;
     const int64_t row = ((int64_t)bh * P.nseg + g) * P.lmax + t;
-    const float li = a.ws[P.lse_off + row];
-    const f32x4 o = *reinterpret_cast<const f32x4*>(a.ws + P.o_off + row * D + d0);
-    if (li > m) {
-      const float c = __builtin_amdgcn_exp2f((m - li) * kLog2e);
-      den *= c;
-      acc *= c;
-      m = li;
-    }
-    const float e = __builtin_amdgcn_exp2f((li - m) * kLog2e);
-    den += e;
-    acc += e * o;
+    li[i] = reinterpret_cast<const float*>(a.ws + P.lse_off)[row];
+    o[i] = load8(reinterpret_cast<const WsT*>(a.ws + P.o_off) + row * D + d0);
   }
+  // Combined log-sum-exp, then the denominator-weighted sum.
+  float m = -INFINITY;
+#pragma unroll
+  for (int i = 0; i < DA_MAX_PATTERNS; ++i) m = fmaxf(m, li[i]);
   const int b = bh / a.H;
   OutT* out = static_cast<OutT*>(a.out) + (((int64_t)b * a.N + p) * a.H + h) * D + d0;
-  float lse_v;
-  if (den > 0.0f) {
-    const float inv = 1.0f / den;
-    store4(out, acc * inv);
+  float lse_v = -INFINITY;
+  f32x8 acc = f32x8{0, 0, 0, 0, 0, 0, 0, 0};
+  if (m != -INFINITY) {
+    float den = 0.0f;
+#pragma unroll
+    for (int i = 0; i < DA_MAX_PATTERNS; ++i) {
+      if (li[i] == -INFINITY) continue;
+      const float e = __builtin_amdgcn_exp2f((li[i] - m) * kLog2e);
+      den += e;
+      acc += e * to_f32(o[i]);
+    }
+    acc *= 1.0f / den;
     lse_v = m + __builtin_amdgcn_logf(den) * kLn2;
-  } else {
-    store4(out, f32x4{0, 0, 0, 0});
-    lse_v = -INFINITY;
   }
+  store8(out, acc);
   if (d0 == 0) a.lse[(int64_t)bh * a.N + p] = lse_v;
+}
+
+template <int D, typename OutT, typename WsT>
+void launch_one(const dim3& grid, hipStream_t stream, const CombArgs& a) {
+  hipLaunchKernelGGL((combine_fwd<D, OutT, WsT>), grid, dim3(kThreads), 0, stream, a);
 }
 
 }  // namespace
@@ -107,7 +139,7 @@ __global__ __launch_bounds__(kThreads) void combine_fwd(CombArgs a) {
 hipError_t launch_combine(const Plan& plan, const void* workspace, void* out, float* lse,
                           hipStream_t stream) {
   CombArgs a;
-  a.ws = static_cast<const float*>(workspace);
+  a.ws = static_cast<const char*>(workspace);
   a.out = out;
   a.lse = lse;
   a.N = static_cast<int32_t>(plan.N);
@@ -121,13 +153,13 @@ hipError_t launch_combine(const Plan& plan, const void* workspace, void* out, fl
       c.fr = make_fastdiv(static_cast<uint32_t>(pp.r));
       c.nseg = static_cast<int32_t>(pp.nseg);
       c.lmax = static_cast<int32_t>(pp.lmax);
-      c.o_off = static_cast<int64_t>(pp.o_off / 4);
-      c.lse_off = static_cast<int64_t>(pp.lse_off / 4);
+      c.o_off = static_cast<int64_t>(pp.o_off);
+      c.lse_off = static_cast<int64_t>(pp.lse_off);
     } else {
       c = CombPat{make_fastdiv(1), make_fastdiv(1), 1, 1, 0, 0};
     }
   }
-  const int rpb = kThreads / (static_cast<int>(plan.D) / 4);
+  const int rpb = kThreads / (static_cast<int>(plan.D) / 8);
   a.chunks = static_cast<int32_t>((plan.N + rpb - 1) / rpb);
   const int64_t blocks = static_cast<int64_t>(a.chunks) * plan.B * plan.H;
   if (blocks >= (int64_t{1} << 31)) return hipErrorInvalidValue;
@@ -135,16 +167,16 @@ hipError_t launch_combine(const Plan& plan, const void* workspace, void* out, fl
   const bool bf = plan.dtype == DA_BF16;
   switch (plan.D) {
     case 32:
-      if (bf) hipLaunchKernelGGL((combine_fwd<32, unsigned short>), grid, dim3(kThreads), 0, stream, a);
-      else hipLaunchKernelGGL((combine_fwd<32, float>), grid, dim3(kThreads), 0, stream, a);
+      if (bf) launch_one<32, unsigned short, _Float16>(grid, stream, a);
+      else launch_one<32, float, float>(grid, stream, a);
       break;
     case 64:
-      if (bf) hipLaunchKernelGGL((combine_fwd<64, unsigned short>), grid, dim3(kThreads), 0, stream, a);
-      else hipLaunchKernelGGL((combine_fwd<64, float>), grid, dim3(kThreads), 0, stream, a);
+      if (bf) launch_one<64, unsigned short, _Float16>(grid, stream, a);
+      else launch_one<64, float, float>(grid, stream, a);
       break;
     case 128:
-      if (bf) hipLaunchKernelGGL((combine_fwd<128, unsigned short>), grid, dim3(kThreads), 0, stream, a);
-      else hipLaunchKernelGGL((combine_fwd<128, float>), grid, dim3(kThreads), 0, stream, a);
+      if (bf) launch_one<128, unsigned short, _Float16>(grid, stream, a);
+      else launch_one<128, float, float>(grid, stream, a);
       break;
     default:
       return hipErrorInvalidValue;

@@ -61,6 +61,10 @@ int make_plan(int64_t B, int64_t N, int64_t H, int64_t D, const da_pattern_t* pa
   p.npat = static_cast<int>(num_patterns);
   p.block_m = block_m_for(p.dtype);
   const int64_t esize = dtype == DA_BF16 ? 2 : 4;
+  // Per-pattern outputs are kept as fp16 for bf16 inputs (they are convex
+  // combinations of v rows, well inside fp16 range, with 3 more mantissa bits
+  // than bf16) and as fp32 for fp32 inputs.
+  const int64_t ws_esize = dtype == DA_BF16 ? 2 : 4;
 
   uint64_t ws = 0;
   int64_t items = 0;
@@ -80,7 +84,7 @@ int make_plan(int64_t B, int64_t N, int64_t H, int64_t D, const da_pattern_t* pa
     items += pp.units * pp.ntiles;
     const uint64_t rows = static_cast<uint64_t>(pp.units) * static_cast<uint64_t>(pp.lmax);
     pp.o_off = ws;
-    ws = align_up(ws + rows * static_cast<uint64_t>(D) * 4);
+    ws = align_up(ws + rows * static_cast<uint64_t>(D) * ws_esize);
     pp.lse_off = ws;
     ws = align_up(ws + rows * 4);
 
@@ -115,8 +119,8 @@ int make_plan(int64_t B, int64_t N, int64_t H, int64_t D, const da_pattern_t* pa
   p.workspace_bytes = ws;
   p.covered_rows = covered;
   p.sparse_flops = static_cast<double>(4.0L * D * pairs);
-  p.bytes_attn = static_cast<double>(covered) * (3.0 * D * esize + (D + 1) * 4.0);
-  p.bytes_combine = static_cast<double>(covered) * (D + 1) * 4.0 +
+  p.bytes_attn = static_cast<double>(covered) * (3.0 * D * esize + D * ws_esize + 4.0);
+  p.bytes_combine = static_cast<double>(covered) * (D * ws_esize + 4.0) +
                     static_cast<double>(B) * N * H * (D * esize + 4.0);
   *out = p;
   return DA_OK;

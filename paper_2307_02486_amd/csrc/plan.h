@@ -42,6 +42,7 @@ struct PatternPlan {
   int64_t units;      // B * H * nseg
   int64_t item_begin; // index of this pattern's first work item
   uint64_t o_off;     // byte offset of the per-pattern output in the workspace
+                      // (fp16 rows for bf16 inputs, fp32 rows for fp32 inputs)
   uint64_t lse_off;   // byte offset of the per-pattern lse in the workspace
 };
 

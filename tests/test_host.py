@@ -73,9 +73,10 @@ def test_plan_accounting_matches_enumeration(wl):
     rows = wl.B * oracle.covered_rows(wl.N, wl.H, wl.patterns)
     assert info["covered_rows"] == rows
     assert info["sparse_flops"] == pytest.approx(flops, rel=1e-12)
-    es = 2 if wl.dtype == "bf16" else 4
-    assert info["bytes_attn"] == rows * (3 * wl.D * es + 4 * (wl.D + 1))
-    assert info["bytes_combine"] == rows * 4 * (wl.D + 1) + wl.B * wl.N * wl.H * (wl.D * es + 4)
+    es = 2 if wl.dtype == "bf16" else 4     # element size of q, k, v, out
+    ws = 2 if wl.dtype == "bf16" else 4     # per-pattern outputs: fp16 or fp32
+    assert info["bytes_attn"] == rows * (3 * wl.D * es + wl.D * ws + 4)
+    assert info["bytes_combine"] == rows * (wl.D * ws + 4) + wl.B * wl.N * wl.H * (wl.D * es + 4)
 
 
 def test_plan_accounting_random_small():
