@@ -53,6 +53,25 @@ def copy_calibration(mib):
     print(json.dumps({"copy_calibration_bytes_each_way": mib * (1 << 20), "launches": 5}), flush=True)
 
 
+def profiled_traffic(workload):
+    """HBM bytes per launch of the attention and combine kernels measured with
+    rocprofv3 FETCH_SIZE / WRITE_SIZE (scaled by a plain copy of known size),
+    or None when the attention kernel's source changed since the measurement."""
+    import hashlib
+    if not os.path.exists(PROFILED_TRAFFIC):
+        return None, None
+    with open(PROFILED_TRAFFIC) as f:
+        rec = json.load(f).get(workload)
+    if not rec:
+        return None, None
+    src = os.path.join(ROOT, "paper_2307_02486_amd", "csrc", "attn_fwd.hip")
+    with open(src, "rb") as f:
+        sha = hashlib.sha256(f.read()).hexdigest()[:16]
+    if sha != rec.get("attn_fwd_hip_sha256_16"):
+        return None, None
+    return rec.get("attention_bytes_per_launch"), rec.get("combine_bytes_per_launch")
+
+
 def cpu_baseline(wl, q, k, v, min_seconds):
     """Time the CPU oracle, as it stands, on whole heads of the same workload
     until at least `min_seconds` have passed; report flops/s over those heads."""
@@ -143,10 +162,7 @@ def main():
     attn_tflops = flops / (ms_attn * 1e-3) / 1e12
     comb_gbs = info["bytes_combine"] / (ms_comb * 1e-3) / 1e9
     peak = PEAK_BF16_TFLOPS if wl.dtype == "bf16" else PEAK_F32_TFLOPS
-    traffic = None
-    if os.path.exists(PROFILED_TRAFFIC):
-        with open(PROFILED_TRAFFIC) as f:
-            traffic = json.load(f).get(wl.name, {}).get("attention_bytes_per_launch")
+    traffic, comb_traffic = profiled_traffic(wl.name)
     res = {
         "metric": METRIC,
         "value": round(tflops, 3),
@@ -166,7 +182,8 @@ def main():
         "attention_stage": {"ms": round(ms_attn, 5), "tflops": round(attn_tflops, 3),
                             "frac_of_mfma_peak": round(attn_tflops / peak, 4)},
         "combine_stage": {"ms": round(ms_comb, 5), "algorithmic_bytes": info["bytes_combine"],
-                          "gbps": round(comb_gbs, 1), "frac_of_hbm_peak": round(comb_gbs / PEAK_HBM_GBS, 4)},
+                          "gbps": round(comb_gbs, 1), "frac_of_hbm_peak": round(comb_gbs / PEAK_HBM_GBS, 4),
+                          "traffic": comb_traffic},
         "roofline": {"bound": "mfma", "achieved": round(attn_tflops, 3), "peak": peak,
                      "unit": "TFLOP/s", "frac": round(attn_tflops / peak, 4), "traffic": traffic},
         "cpu_baseline": None,
