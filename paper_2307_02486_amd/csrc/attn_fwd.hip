@@ -23,7 +23,6 @@ namespace da {
 namespace {
 
 typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
-typedef __bf16 bf16x2 __attribute__((ext_vector_type(2)));
 typedef float f32x16 __attribute__((ext_vector_type(16)));
 typedef float f32x4 __attribute__((ext_vector_type(4)));
 typedef _Float16 f16x4 __attribute__((ext_vector_type(4)));
@@ -120,11 +119,6 @@ constexpr float kRescaleSlack = 8.0f;
 #ifndef DA_QK_GROUP
 #define DA_QK_GROUP 2
 #endif
-// Scores from q pre-multiplied by scale*log2(e) and rounded to bf16 (1), or
-// from q as given with the scale applied per score in fp32 (0).
-#ifndef DA_PRESCALED_Q
-#define DA_PRESCALED_Q 1
-#endif
 template <int D> struct KeyTile { static constexpr int value = D <= 64 ? DA_KEY_TILE_SMALL_D : 64; };
 
 // Position of key `key` inside a transposed V row: within each group of 16
@@ -196,7 +190,6 @@ __global__ __launch_bounds__(kThreads) void attn_fwd_bf16(AttnArgs a) {
 #pragma unroll
     for (int c = 0; c < KC; ++c) {
       u32x4 x = q_valid ? load16(qp + 16 * c) : u32x4{0, 0, 0, 0};
-#if DA_PRESCALED_Q
       // q * scale * log2(e), rounded to bf16: the MFMA then yields scores in
       // log2 units and the exponent needs no per-score multiply.
 #pragma unroll
@@ -204,9 +197,6 @@ __global__ __launch_bounds__(kThreads) void attn_fwd_bf16(AttnArgs a) {
         const unsigned bits = (x[e >> 1] >> (16 * (e & 1))) << 16;
         qreg[c][e] = (__bf16)(__builtin_bit_cast(float, bits) * a.scale_log2);
       }
-#else
-      qreg[c] = __builtin_bit_cast(bf16x8, x);
-#endif
     }
   }
 
@@ -296,12 +286,8 @@ __global__ __launch_bounds__(kThreads) void attn_fwd_bf16(AttnArgs a) {
   f32x16 acc_o[DB];
 #pragma unroll
   for (int db = 0; db < DB; ++db) acc_o[db] = f32x16{};
-#if DA_PRESCALED_Q
   float m_run = 0.0f;     // reference max of scaled scores (log2 domain), set by tile 0
   f32x16 negm = f32x16{}; // -m_run in every slot: the initial value of each S' block
-#else
-  float m_run = kNegBig;  // reference max of scaled scores (log2 domain)
-#endif
   float l_run = 0.0f;     // this half-wave's share of the running denominator
 
   const int kv_end = a.causal ? qend : L;
@@ -334,24 +320,14 @@ __global__ __launch_bounds__(kThreads) void attn_fwd_bf16(AttnArgs a) {
             kf[g][c] = *reinterpret_cast<const u32x4*>(
                 &sm.k[cur][((kb0 + g) * 32 + qr) * Smem::KSTR + 16 * c + 8 * hi]);
         __builtin_amdgcn_sched_barrier(0);  // keep the reads ahead of the MFMAs
-#ifdef DA_SETPRIO
-        __builtin_amdgcn_s_setprio(1);
-#endif
 #pragma unroll
         for (int g = 0; g < QG; ++g) {
-#if DA_PRESCALED_Q
           acc_s[kb0 + g] = negm;  // scores start at -m: S' = q'k - m
-#else
-          acc_s[kb0 + g] = f32x16{};
-#endif
 #pragma unroll
           for (int c = 0; c < KC; ++c)
             acc_s[kb0 + g] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(
                 __builtin_bit_cast(bf16x8, kf[g][c]), qreg[c], acc_s[kb0 + g], 0, 0, 0);
         }
-#ifdef DA_SETPRIO
-        __builtin_amdgcn_s_setprio(0);
-#endif
       }
       // Mask keys after the query (causal) and past the segment's end.
       if ((a.causal && k0 + BN - 1 > wq_lo) || k0 + BN > L) {
@@ -368,7 +344,6 @@ __global__ __launch_bounds__(kThreads) void attn_fwd_bf16(AttnArgs a) {
       for (int kb = 0; kb < SB; ++kb)
 #pragma unroll
         for (int j = 0; j < 16; j += 2) mx = fmaxf(mx, fmaxf(acc_s[kb][j], acc_s[kb][j + 1]));
-#if DA_PRESCALED_Q
       mx = fmaxf(mx, other_half(mx));  // already relative to m_run, log2 units
       // Lazy rescale: the first tile fixes the reference max; later tiles move
       // it only when some row of the wave would see probabilities above
@@ -389,23 +364,11 @@ __global__ __launch_bounds__(kThreads) void attn_fwd_bf16(AttnArgs a) {
 #pragma unroll
         for (int j = 0; j < 16; ++j) negm[j] = -m_run;
       }
-#else
-      mx = fmaxf(mx, other_half(mx)) * a.scale_log2;
-      // Lazy rescale: move the reference max only when some row of the wave
-      // would otherwise see probabilities above 2^kRescaleSlack.
-      if (__any(mx > m_run + kRescaleSlack)) {
-        const float m_new = fmaxf(m_run, mx);
-        const float alpha = __builtin_amdgcn_exp2f(m_run - m_new);
-        m_run = m_new;
-        l_run *= alpha;
-#pragma unroll
-        for (int db = 0; db < DB; ++db)
-#pragma unroll
-          for (int j = 0; j < 16; ++j) acc_o[db][j] *= alpha;
-      }
-#endif
-      // P = exp2(scale*log2e*S - m); bf16 P feeds the PV MFMA and the row sum.
-      // The V^T fragments of a 32-key block are requested before its exps.
+      // P = exp2(S'); bf16 P feeds the PV MFMA.  The row sums are taken in
+      // fp32 with plain adds (dot-product instructions would not issue while
+      // other waves' MFMAs run).  The V^T fragments of a 32-key block are
+      // requested before its exps.
+      float lp[4] = {0.0f, 0.0f, 0.0f, 0.0f};
 #pragma unroll
       for (int kb = 0; kb < SB; ++kb) {
         u32x4 vf[2][DB];
@@ -420,16 +383,10 @@ __global__ __launch_bounds__(kThreads) void attn_fwd_bf16(AttnArgs a) {
         for (int kk = 0; kk < 2; ++kk) {
           bf16x8 pb;
 #pragma unroll
-          for (int e = 0; e < 8; ++e)
-#if DA_PRESCALED_Q
-            pb[e] = (__bf16)__builtin_amdgcn_exp2f(acc_s[kb][8 * kk + e]);
-#else
-            pb[e] = (__bf16)__builtin_amdgcn_exp2f(fmaf(acc_s[kb][8 * kk + e], a.scale_log2, -m_run));
-#endif
-#pragma unroll
-          for (int e = 0; e < 8; e += 2) {
-            bf16x2 pr = {pb[e], pb[e + 1]};
-            l_run = __builtin_amdgcn_fdot2_f32_bf16(pr, bf16x2{(__bf16)1.0f, (__bf16)1.0f}, l_run, false);
+          for (int e = 0; e < 8; ++e) {
+            const float pe = __builtin_amdgcn_exp2f(acc_s[kb][8 * kk + e]);
+            lp[e & 3] += pe;
+            pb[e] = (__bf16)pe;
           }
 #pragma unroll
           for (int db = 0; db < DB; ++db)
@@ -437,6 +394,7 @@ __global__ __launch_bounds__(kThreads) void attn_fwd_bf16(AttnArgs a) {
                                                                 pb, acc_o[db], 0, 0, 0);
         }
       }
+      l_run += (lp[0] + lp[1]) + (lp[2] + lp[3]);
     }
     if (more) store_tile(cur ^ 1);
     __syncthreads();
