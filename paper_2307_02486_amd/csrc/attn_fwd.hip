@@ -100,42 +100,38 @@ __device__ inline bool decode_item(const AttnArgs& a, int bid, int block_m, Item
 // ---------------------------------------------------------------------------
 // bf16 MFMA kernel
 // ---------------------------------------------------------------------------
-#ifndef DA_BF16_WAVES
-#define DA_BF16_WAVES 4
-#endif
-constexpr int kThreads = 64 * DA_BF16_WAVES;  // waves of 32 query rows each
-constexpr int kBM = 32 * DA_BF16_WAVES;       // query rows per work item
+constexpr int kThreads = 256;  // four waves of 32 query rows each
+constexpr int kBM = 128;       // query rows per work item
+constexpr int kBN = 64;        // keys per K/V tile
 // A row's running max is raised only when a tile's max exceeds it by more than
 // this (log2 units); until then probabilities may reach 2^kRescaleSlack, which
 // bf16 and the fp32 sums hold exactly as well as values below 1.
 constexpr float kRescaleSlack = 8.0f;
 
-// Keys per K/V tile for a head dim: 128 where the registers allow it.
-#ifndef DA_KEY_TILE_SMALL_D
-#define DA_KEY_TILE_SMALL_D 64
-#endif
-// 32-key blocks of S^T whose K fragments are read from LDS together, before
-// their MFMAs, so LDS latency is paid once per group rather than per MFMA.
-#ifndef DA_QK_GROUP
-#define DA_QK_GROUP 2
-#endif
-template <int D> struct KeyTile { static constexpr int value = D <= 64 ? DA_KEY_TILE_SMALL_D : 64; };
-
-// Position of key `key` inside a transposed V row: within each group of 16
-// keys, keys {0-3, 8-11} come first and {4-7, 12-15} second, which is the
-// order in which the upper and lower half-waves hold them after S^T.
-__device__ inline int vt_pos(int key) {
-  const int k16 = key & 15;
-  return (key & ~15) | (((k16 >> 2) & 1) << 3) | ((k16 >> 3) << 2) | (k16 & 3);
-}
-
-template <int D, int BN>
-struct SmemBf16 {
-  static constexpr int KSTR = D + 8;    // row pitch (elements) of a K tile
-  static constexpr int VSTR = BN + 8;   // row pitch (elements) of a V^T tile
-  u16 k[2][BN * KSTR];                  // double-buffered
-  u16 vt[2][D * VSTR];
+// K and V tiles live in LDS row-major (kBN rows of D bf16), without padding:
+// a row is D/8 16-byte slots and logical slot c of row k is stored at slot
+// c ^ (k & swz), so eight consecutive rows read at one logical slot hit eight
+// different bank groups.
+template <int D>
+struct TileLayout {
+  static constexpr int kSlots = D / 8;                     // 16-byte slots per row
+  static constexpr int kSwz = kSlots < 8 ? kSlots - 1 : 7; // swizzle mask
+  static constexpr int kRowBytes = D * 2;
+  static constexpr int kTileBytes = kBN * kRowBytes;
+  __device__ static int offset(int row, int slot) {        // byte offset of a slot
+    return row * kRowBytes + ((slot ^ (row & kSwz)) << 4);
+  }
 };
+
+template <int D>
+struct SmemBf16 {
+  __attribute__((aligned(16))) u16 k[2][kBN * D];  // double-buffered K tiles
+  __attribute__((aligned(16))) u16 v[2][kBN * D];  // double-buffered V tiles
+};
+
+typedef __attribute__((address_space(3))) void lds_void;
+typedef __bf16 bf16x4 __attribute__((__vector_size__(4 * sizeof(__bf16))));
+typedef __attribute__((address_space(3))) bf16x4 lds_bf16x4;
 
 __device__ inline u32x4 load16(const u16* p) { return *reinterpret_cast<const u32x4*>(p); }
 
@@ -151,20 +147,21 @@ __device__ inline float other_half(float x) {
 // no swizzle); with stride 0 the size field is a byte count and reads at or
 // beyond it return zero.
 constexpr int kBufferFlags = 0x00020000;
+// s_waitcnt immediate: vmcnt(0), expcnt and lgkmcnt left at their maxima.
+constexpr int kWaitVmcnt0 = 0x0F70;
 
 template <int D, bool kBufferLoads>
 __global__ __launch_bounds__(kThreads) void attn_fwd_bf16(AttnArgs a) {
   static_assert(D % 32 == 0, "head dim must be a multiple of 32");
-  constexpr int BN = KeyTile<D>::value;
+  constexpr int BN = kBN;
   constexpr int KC = D / 16;  // MFMA k-steps over the head dim
   constexpr int DB = D / 32;  // 32-wide blocks of the head dim in O^T
   constexpr int SB = BN / 32; // 32-key blocks of S^T per tile
-  constexpr int KTASKS = BN * D / 8;                        // 16-B K chunks per tile
-  constexpr int KT = (KTASKS + kThreads - 1) / kThreads;    // K chunks per thread
-  constexpr int VTASKS = (BN / 2) * (D / 8);                // (key pair, 8-wide chunk) V tasks
-  constexpr int VT = (VTASKS + kThreads - 1) / kThreads;    // V tasks per thread
-  using Smem = SmemBf16<D, BN>;
-  __shared__ __attribute__((aligned(16))) Smem sm;
+  using TL = TileLayout<D>;
+  // A wave's load instruction fills 64 consecutive 16-byte LDS slots.
+  constexpr int kLoadsPerWave = BN * TL::kSlots / 64 / (kThreads / 64);
+  static_assert(kLoadsPerWave >= 1, "tile too small for four waves");
+  __shared__ SmemBf16<D> sm;
 
   Item it;
   if (!decode_item(a, __builtin_amdgcn_workgroup_id_x(), kBM, it)) return;
@@ -173,7 +170,7 @@ __global__ __launch_bounds__(kThreads) void attn_fwd_bf16(AttnArgs a) {
 
   const int tid = __builtin_amdgcn_workitem_id_x();
   const int lane = tid & 63;
-  const int wv = tid >> 6;
+  const int wv = __builtin_amdgcn_readfirstlane(tid >> 6);  // wave index (uniform)
   const int qr = lane & 31;   // query column of this lane in S^T / O^T
   const int hi = lane >> 5;   // half-wave
   const int L = it.L;
@@ -183,15 +180,15 @@ __global__ __launch_bounds__(kThreads) void attn_fwd_bf16(AttnArgs a) {
   const bool q_valid = tq_row < L;
   const int64_t row_step = it.rstride * D;  // elements between consecutive kept rows
 
-  // Q^T operand: lane holds query tq_row, head-dim slice [16c + 8hi, +8).
+  // Q^T operand: lane holds query tq_row, head-dim slice [16c + 8hi, +8),
+  // multiplied by scale * log2(e) and rounded to bf16: the MFMA then yields
+  // scores in log2 units and the exponent needs no per-score multiply.
   bf16x8 qreg[KC];
   {
     const u16* qp = qg + (it.row0 + (int64_t)tq_row * it.rstride) * D + 8 * hi;
 #pragma unroll
     for (int c = 0; c < KC; ++c) {
       u32x4 x = q_valid ? load16(qp + 16 * c) : u32x4{0, 0, 0, 0};
-      // q * scale * log2(e), rounded to bf16: the MFMA then yields scores in
-      // log2 units and the exponent needs no per-score multiply.
 #pragma unroll
       for (int e = 0; e < 8; ++e) {
         const unsigned bits = (x[e >> 1] >> (16 * (e & 1))) << 16;
@@ -200,85 +197,51 @@ __global__ __launch_bounds__(kThreads) void attn_fwd_bf16(AttnArgs a) {
     }
   }
 
-  // Fixed per-thread roles in the tile loads:
-  //  K chunk i: key (tid + 256i) / (D/8), head-dim chunk (tid + 256i) % (D/8)
-  //  V task i:  keys 2kp, 2kp+1 with kp = (tid + 256i) % (BN/2), chunk (tid + 256i) / (BN/2)
-  // With kBufferLoads, a tile is read through a buffer resource whose base is
-  // the tile's first kept row and whose size ends at the segment's last kept
-  // row: each thread keeps a fixed 32-bit offset, and rows past the end read
-  // as zero without any per-load test.  Otherwise 64-bit pointers and tests.
-  int kkey[KT], kdc[KT];
+  // Tile loads go straight from HBM to LDS (no registers, no LDS stores).
+  // Load i of this wave fills LDS slots [64 (wv*kLoadsPerWave + i), +64): lane
+  // l takes slot s = 64 (wv*kLoadsPerWave + i) + l, i.e. row s / kSlots and
+  // physical slot s % kSlots, and fetches the logical slot stored there.
+  int lrow[kLoadsPerWave], lslot[kLoadsPerWave];
 #pragma unroll
-  for (int i = 0; i < KT; ++i) {
-    const int task = min(tid + i * kThreads, KTASKS - 1);
-    kkey[i] = task / (D / 8);
-    kdc[i] = task % (D / 8);
-  }
-  int vkey[VT], vdc[VT];
-#pragma unroll
-  for (int i = 0; i < VT; ++i) {
-    const int task = min(tid + i * kThreads, VTASKS - 1);
-    vkey[i] = 2 * (task % (BN / 2));
-    vdc[i] = task / (BN / 2);
+  for (int i = 0; i < kLoadsPerWave; ++i) {
+    const int s = 64 * (wv * kLoadsPerWave + i) + lane;
+    lrow[i] = s / TL::kSlots;
+    lslot[i] = (s % TL::kSlots) ^ (lrow[i] & TL::kSwz);
   }
   const u16* kbase = static_cast<const u16*>(a.k) + it.row0 * D;
   const u16* vbase = static_cast<const u16*>(a.v) + it.row0 * D;
   const int64_t tile_step = row_step * BN;
-
-  u32x4 rk[KT], rv0[VT], rv1[VT];
-  auto load_tile = [&](int jt) {
+  auto load_tile = [&](int jt, int buf) {
     const int k0 = jt * BN;
+    char* kl = reinterpret_cast<char*>(&sm.k[buf][0]);
+    char* vl = reinterpret_cast<char*>(&sm.v[buf][0]);
     if constexpr (kBufferLoads) {
+      // Buffer resources based at the tile's first kept row, sized to end at
+      // the segment's last kept row: rows past it arrive as zeros.
       const uint64_t row_bytes = static_cast<uint64_t>(row_step) * 2;
       const uint64_t valid = static_cast<uint64_t>(L - k0) * row_bytes;
       const int nrec = static_cast<int>(valid < 0x7fffffffull ? valid : 0x7fffffffull);
-      const __amdgpu_buffer_rsrc_t rk_src = __builtin_amdgcn_make_buffer_rsrc(
+      const __amdgpu_buffer_rsrc_t ksrc = __builtin_amdgcn_make_buffer_rsrc(
           const_cast<u16*>(kbase + tile_step * jt), 0, nrec, kBufferFlags);
-      const __amdgpu_buffer_rsrc_t rv_src = __builtin_amdgcn_make_buffer_rsrc(
+      const __amdgpu_buffer_rsrc_t vsrc = __builtin_amdgcn_make_buffer_rsrc(
           const_cast<u16*>(vbase + tile_step * jt), 0, nrec, kBufferFlags);
 #pragma unroll
-      for (int i = 0; i < KT; ++i)
-        rk[i] = __builtin_amdgcn_raw_buffer_load_b128(
-            rk_src, static_cast<int>(kkey[i] * row_bytes) + kdc[i] * 16, 0, 0);
-#pragma unroll
-      for (int i = 0; i < VT; ++i) {
-        const int off = static_cast<int>(vkey[i] * row_bytes) + vdc[i] * 16;
-        rv0[i] = __builtin_amdgcn_raw_buffer_load_b128(rv_src, off, 0, 0);
-        rv1[i] = __builtin_amdgcn_raw_buffer_load_b128(rv_src, off + static_cast<int>(row_bytes), 0, 0);
+      for (int i = 0; i < kLoadsPerWave; ++i) {
+        const int off = static_cast<int>(lrow[i] * row_bytes) + lslot[i] * 16;
+        const int lds_off = 1024 * (wv * kLoadsPerWave + i);
+        __builtin_amdgcn_raw_ptr_buffer_load_lds(ksrc, (lds_void*)(kl + lds_off), 16, off, 0, 0, 0);
+        __builtin_amdgcn_raw_ptr_buffer_load_lds(vsrc, (lds_void*)(vl + lds_off), 16, off, 0, 0, 0);
       }
     } else {
-      const int64_t off = tile_step * jt;
+      // 64-bit addresses; rows past the segment's end re-read its last row
+      // (those keys are masked, and their probabilities are zero).
 #pragma unroll
-      for (int i = 0; i < KT; ++i)
-        rk[i] = k0 + kkey[i] < L ? load16(kbase + off + kkey[i] * row_step + kdc[i] * 8) : u32x4{0, 0, 0, 0};
-#pragma unroll
-      for (int i = 0; i < VT; ++i) {
-        const int t = k0 + vkey[i];
-        const u16* vp = vbase + off + vkey[i] * row_step + vdc[i] * 8;
-        rv0[i] = t < L ? load16(vp) : u32x4{0, 0, 0, 0};
-        rv1[i] = t + 1 < L ? load16(vp + row_step) : u32x4{0, 0, 0, 0};
-      }
-    }
-  };
-  auto store_tile = [&](int buf) {
-#pragma unroll
-    for (int i = 0; i < KT; ++i) {
-      const int task = tid + i * kThreads;
-      if (KTASKS % kThreads == 0 || task < KTASKS)
-        *reinterpret_cast<u32x4*>(&sm.k[buf][(task / (D / 8)) * Smem::KSTR + (task % (D / 8)) * 8]) = rk[i];
-    }
-#pragma unroll
-    for (int i = 0; i < VT; ++i) {
-      const int task = tid + i * kThreads;
-      if (VTASKS % kThreads == 0 || task < VTASKS) {
-        u16* dst = &sm.vt[buf][(task / (BN / 2)) * 8 * Smem::VSTR + vt_pos(2 * (task % (BN / 2)))];
-#pragma unroll
-        for (int e = 0; e < 8; ++e) {
-          // (key 2kp, key 2kp+1) of head-dim element dc*8 + e, as one 32-bit word
-          const unsigned sel = (e & 1) ? 0x07060302u : 0x05040100u;
-          *reinterpret_cast<unsigned*>(dst + e * Smem::VSTR) =
-              __builtin_amdgcn_perm(rv1[i][e >> 1], rv0[i][e >> 1], sel);
-        }
+      for (int i = 0; i < kLoadsPerWave; ++i) {
+        const int64_t row = min(k0 + lrow[i], L - 1);
+        const int64_t off = row * row_step + lslot[i] * 8;
+        const int lds_off = 1024 * (wv * kLoadsPerWave + i);
+        __builtin_amdgcn_global_load_lds(kbase + off, (lds_void*)(kl + lds_off), 16, 0, 0);
+        __builtin_amdgcn_global_load_lds(vbase + off, (lds_void*)(vl + lds_off), 16, 0, 0);
       }
     }
   };
@@ -294,40 +257,42 @@ __global__ __launch_bounds__(kThreads) void attn_fwd_bf16(AttnArgs a) {
   const int ntile = (kv_end + BN - 1) / BN;
   const int wq_lo = q0 + wv * 32;  // smallest query of this wave
   const int lim = a.causal ? min(tq_row, L - 1) : L - 1;  // last visible key of this lane
+  // Lane roles in the transposed V reads (ds_read_b64_tr_b16): within each
+  // 16-lane group, lane 4r + cb supplies the address of key row r, head-dim
+  // columns 4cb..4cb+3, and receives one column across the four rows.
+  const int tr_r = (lane & 15) >> 2;
+  const int tr_d = ((lane >> 4) & 1) * 16 + (lane & 3) * 4;
 
-  load_tile(0);
-  store_tile(0);
+  load_tile(0, 0);
+  __builtin_amdgcn_s_waitcnt(kWaitVmcnt0);
   __syncthreads();
   for (int jt = 0; jt < ntile; ++jt) {
     const int cur = jt & 1;
     const int k0 = jt * BN;
     const bool more = jt + 1 < ntile;
-    if (more) load_tile(jt + 1);
+    if (more) load_tile(jt + 1, cur ^ 1);
+    const char* kl = reinterpret_cast<const char*>(&sm.k[cur][0]);
+    const char* vl = reinterpret_cast<const char*>(&sm.v[cur][0]);
 
     // Tiles entirely after this wave's queries are skipped (causal).
     if (!(a.causal && k0 > wq_lo + 31)) {
-      // S^T = K Q^T, one 32x32 block per 32 keys; the K fragments of a group
-      // of blocks are all requested from LDS before the group's MFMAs.
+      // S^T = K Q^T, one 32x32 block per 32 keys; all K fragments of the tile
+      // are requested from LDS before the MFMAs.
       f32x16 acc_s[SB];
-      constexpr int QG = DA_QK_GROUP < SB ? DA_QK_GROUP : SB;
+      u32x4 kf[SB][KC];
 #pragma unroll
-      for (int kb0 = 0; kb0 < SB; kb0 += QG) {
-        u32x4 kf[QG][KC];
+      for (int kb = 0; kb < SB; ++kb)
 #pragma unroll
-        for (int g = 0; g < QG; ++g)
+        for (int c = 0; c < KC; ++c)
+          kf[kb][c] = *reinterpret_cast<const u32x4*>(kl + TL::offset(kb * 32 + qr, 2 * c + hi));
+      __builtin_amdgcn_sched_barrier(0);  // keep the reads ahead of the MFMAs
 #pragma unroll
-          for (int c = 0; c < KC; ++c)
-            kf[g][c] = *reinterpret_cast<const u32x4*>(
-                &sm.k[cur][((kb0 + g) * 32 + qr) * Smem::KSTR + 16 * c + 8 * hi]);
-        __builtin_amdgcn_sched_barrier(0);  // keep the reads ahead of the MFMAs
+      for (int kb = 0; kb < SB; ++kb) {
+        acc_s[kb] = negm;  // scores start at -m: S' = q'k - m
 #pragma unroll
-        for (int g = 0; g < QG; ++g) {
-          acc_s[kb0 + g] = negm;  // scores start at -m: S' = q'k - m
-#pragma unroll
-          for (int c = 0; c < KC; ++c)
-            acc_s[kb0 + g] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(
-                __builtin_bit_cast(bf16x8, kf[g][c]), qreg[c], acc_s[kb0 + g], 0, 0, 0);
-        }
+        for (int c = 0; c < KC; ++c)
+          acc_s[kb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(__builtin_bit_cast(bf16x8, kf[kb][c]), qreg[c],
+                                                              acc_s[kb], 0, 0, 0);
       }
       // Mask keys after the query (causal) and past the segment's end.
       if ((a.causal && k0 + BN - 1 > wq_lo) || k0 + BN > L) {
@@ -364,20 +329,30 @@ __global__ __launch_bounds__(kThreads) void attn_fwd_bf16(AttnArgs a) {
 #pragma unroll
         for (int j = 0; j < 16; ++j) negm[j] = -m_run;
       }
-      // P = exp2(S'); bf16 P feeds the PV MFMA.  The row sums are taken in
-      // fp32 with plain adds (dot-product instructions would not issue while
-      // other waves' MFMAs run).  The V^T fragments of a 32-key block are
-      // requested before its exps.
+      // P = exp2(S'); bf16 P feeds the PV MFMA.  Row sums are taken in fp32
+      // with plain adds (dot-product instructions would not issue while other
+      // waves' MFMAs run).  The A operand V^T comes from the row-major V tile
+      // through transposed LDS reads: for MFMA step (kb, kk) the lane's eight
+      // keys are kb*32 + 16kk + 4hi + {0..3} and the same + 8, matching the
+      // keys its half-wave holds in S^T.
       float lp[4] = {0.0f, 0.0f, 0.0f, 0.0f};
 #pragma unroll
       for (int kb = 0; kb < SB; ++kb) {
-        u32x4 vf[2][DB];
+        bf16x8 vf[2][DB];
 #pragma unroll
         for (int kk = 0; kk < 2; ++kk)
 #pragma unroll
-          for (int db = 0; db < DB; ++db)
-            vf[kk][db] = *reinterpret_cast<const u32x4*>(
-                &sm.vt[cur][(db * 32 + qr) * Smem::VSTR + (kb * 2 + kk) * 16 + 8 * hi]);
+          for (int db = 0; db < DB; ++db) {
+            const int d = db * 32 + tr_d;
+#pragma unroll
+            for (int t = 0; t < 2; ++t) {
+              const int key = kb * 32 + 16 * kk + 8 * t + 4 * hi + tr_r;
+              const bf16x4 h = __builtin_amdgcn_ds_read_tr16_b64_v4bf16(
+                  (lds_bf16x4*)(vl + TL::offset(key, d >> 3) + (d & 7) * 2));
+#pragma unroll
+              for (int e = 0; e < 4; ++e) vf[kk][db][4 * t + e] = h[e];
+            }
+          }
         __builtin_amdgcn_sched_barrier(0);  // keep the reads ahead of the exps
 #pragma unroll
         for (int kk = 0; kk < 2; ++kk) {
@@ -390,13 +365,14 @@ __global__ __launch_bounds__(kThreads) void attn_fwd_bf16(AttnArgs a) {
           }
 #pragma unroll
           for (int db = 0; db < DB; ++db)
-            acc_o[db] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(__builtin_bit_cast(bf16x8, vf[kk][db]),
-                                                                pb, acc_o[db], 0, 0, 0);
+            acc_o[db] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(vf[kk][db], pb, acc_o[db], 0, 0, 0);
         }
       }
       l_run += (lp[0] + lp[1]) + (lp[2] + lp[3]);
     }
-    if (more) store_tile(cur ^ 1);
+    // The next tile's loads have landed in LDS and every wave is done with
+    // this tile before anyone moves on.
+    __builtin_amdgcn_s_waitcnt(kWaitVmcnt0);
     __syncthreads();
   }
 
