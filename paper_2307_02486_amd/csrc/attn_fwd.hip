@@ -102,7 +102,10 @@ __device__ inline bool decode_item(const AttnArgs& a, int bid, int block_m, Item
 // ---------------------------------------------------------------------------
 constexpr int kThreads = 256;  // four waves of 32 query rows each
 constexpr int kBM = 128;       // query rows per work item
-constexpr int kBN = 64;        // keys per K/V tile
+#ifndef DA_KEY_TILE
+#define DA_KEY_TILE 64
+#endif
+constexpr int kBN = DA_KEY_TILE;  // keys per K/V tile
 // A row's running max is raised only when a tile's max exceeds it by more than
 // this (log2 units); until then probabilities may reach 2^kRescaleSlack, which
 // bf16 and the fp32 sums hold exactly as well as values below 1.
@@ -276,23 +279,27 @@ __global__ __launch_bounds__(kThreads) void attn_fwd_bf16(AttnArgs a) {
 
     // Tiles entirely after this wave's queries are skipped (causal).
     if (!(a.causal && k0 > wq_lo + 31)) {
-      // S^T = K Q^T, one 32x32 block per 32 keys; all K fragments of the tile
-      // are requested from LDS before the MFMAs.
+      // S^T = K Q^T, one 32x32 block per 32 keys; the K fragments of a group
+      // of QG blocks are requested from LDS before the group's MFMAs.
+      constexpr int QG = (D <= 64 ? SB : 1);
       f32x16 acc_s[SB];
-      u32x4 kf[SB][KC];
 #pragma unroll
-      for (int kb = 0; kb < SB; ++kb)
+      for (int kb0 = 0; kb0 < SB; kb0 += QG) {
+        u32x4 kf[QG][KC];
 #pragma unroll
-        for (int c = 0; c < KC; ++c)
-          kf[kb][c] = *reinterpret_cast<const u32x4*>(kl + TL::offset(kb * 32 + qr, 2 * c + hi));
-      __builtin_amdgcn_sched_barrier(0);  // keep the reads ahead of the MFMAs
+        for (int g = 0; g < QG; ++g)
 #pragma unroll
-      for (int kb = 0; kb < SB; ++kb) {
-        acc_s[kb] = negm;  // scores start at -m: S' = q'k - m
+          for (int c = 0; c < KC; ++c)
+            kf[g][c] = *reinterpret_cast<const u32x4*>(kl + TL::offset((kb0 + g) * 32 + qr, 2 * c + hi));
+        __builtin_amdgcn_sched_barrier(0);  // keep the reads ahead of the MFMAs
 #pragma unroll
-        for (int c = 0; c < KC; ++c)
-          acc_s[kb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(__builtin_bit_cast(bf16x8, kf[kb][c]), qreg[c],
-                                                              acc_s[kb], 0, 0, 0);
+        for (int g = 0; g < QG; ++g) {
+          acc_s[kb0 + g] = negm;  // scores start at -m: S' = q'k - m
+#pragma unroll
+          for (int c = 0; c < KC; ++c)
+            acc_s[kb0 + g] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(__builtin_bit_cast(bf16x8, kf[g][c]),
+                                                                     qreg[c], acc_s[kb0 + g], 0, 0, 0);
+        }
       }
       // Mask keys after the query (causal) and past the segment's end.
       if ((a.causal && k0 + BN - 1 > wq_lo) || k0 + BN > L) {
