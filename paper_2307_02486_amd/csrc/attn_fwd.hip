@@ -17,6 +17,9 @@
 // inputs, where accuracy rather than speed is the point.
 #include <hip/hip_runtime.h>
 
+#include <algorithm>
+#include <type_traits>
+
 #include "kernels.h"
 
 namespace da {
@@ -27,6 +30,7 @@ typedef float f32x16 __attribute__((ext_vector_type(16)));
 typedef float f32x4 __attribute__((ext_vector_type(4)));
 typedef _Float16 f16x4 __attribute__((ext_vector_type(4)));
 typedef unsigned int u32x4 __attribute__((ext_vector_type(4)));
+typedef unsigned int u32x2 __attribute__((ext_vector_type(2)));
 typedef unsigned short u16;
 
 constexpr float kLn2 = 0.693147180559945309f;
@@ -47,6 +51,7 @@ struct AttnArgs {
   int32_t B, N, H, npat, causal, total_items;
   float scale_log2;  // softmax scale times log2(e): scores go to exp2 directly
   PatArgs pat[DA_MAX_PATTERNS];
+  int8_t order[DA_MAX_PATTERNS];  // patterns by query tiles per unit, most first
 };
 
 // One attention work item: which segment of which pattern, and which query tile.
@@ -60,28 +65,58 @@ struct Item {
   int64_t rstride; // row-index step between consecutive kept rows (r*H)
 };
 
-// Work items are ordered pattern by pattern; inside a pattern, unit by unit
-// (segment fastest), and inside a unit the query tiles run from the last (the
-// longest under a causal mask) to the first.  Workgroups are handed to the
-// eight XCDs round-robin (launch index mod 8), so launch index x is mapped to
-// XCD c = x mod 8 and the units with index = c (mod 8) are given to that XCD:
-// the query tiles of one segment then run on one XCD, close together in time,
-// and its K/V rows are fetched into that XCD's L2 once.
+// Workgroups are handed to the eight XCDs round-robin (launch index mod 8),
+// so launch index x is mapped to XCD c = x mod 8 and the units with index = c
+// (mod 8) are given to that XCD: the query tiles of one segment run on one
+// XCD and its K/V rows are fetched into that XCD's L2 once.  On each XCD the
+// items come in two phases.  First, pattern by pattern (those with the most
+// query tiles per segment first) and unit by unit, the query tiles from the
+// last (the longest under a causal mask) down to tile kShortTiles, so the
+// tiles of a segment run close together in time.  Then
+// the first kShortTiles query tiles of every unit, level by level from tile
+// kShortTiles - 1 down to tile 0: the shortest items are dispatched last and
+// fill the gaps as the longer ones drain.
+constexpr int kShortTiles = 3;
+
+// Number of units of a pattern that XCD c owns.
+__device__ inline int units_on_xcd(const PatArgs& P, int c) {
+  return P.units > c ? (P.units - c + 7) >> 3 : 0;
+}
+
 __device__ inline bool decode_item(const AttnArgs& a, int bid, int block_m, Item& it) {
   const int c = bid & 7;
   int slot = bid >> 3;
-  int pi = 0;
-  for (;; ++pi) {
-    if (pi >= a.npat) return false;
-    const PatArgs& P = a.pat[pi];
-    const int n = (P.units > c ? (P.units - c + 7) >> 3 : 0) * P.ntiles;
-    if (slot < n) break;
+  int pi = -1, j = 0, tq = 0;
+  for (int o = 0; o < a.npat; ++o) {
+    const int p = a.order[o];
+    const PatArgs& P = a.pat[p];
+    const int nlong = P.ntiles > kShortTiles ? P.ntiles - kShortTiles : 0;
+    const int n = units_on_xcd(P, c) * nlong;
+    if (slot < n) {
+      pi = p;
+      j = slot / nlong;
+      tq = P.ntiles - 1 - (slot - j * nlong);
+      break;
+    }
     slot -= n;
   }
+  for (int t = kShortTiles - 1; pi < 0 && t >= 0; --t) {
+    for (int p = 0; p < a.npat; ++p) {
+      const PatArgs& P = a.pat[p];
+      const int n = P.ntiles > t ? units_on_xcd(P, c) : 0;
+      if (slot < n) {
+        pi = p;
+        j = slot;
+        tq = t;
+        break;
+      }
+      slot -= n;
+    }
+  }
+  if (pi < 0) return false;
   const PatArgs& P = a.pat[pi];
-  const int j = slot / P.ntiles;
   const int unit = c + 8 * j;
-  it.tq = P.ntiles - 1 - (slot - j * P.ntiles);
+  it.tq = tq;
   it.pi = pi;
   it.unit = unit;
   it.g = unit % P.nseg;
@@ -133,8 +168,6 @@ struct SmemBf16 {
 };
 
 typedef __attribute__((address_space(3))) void lds_void;
-typedef __bf16 bf16x4 __attribute__((__vector_size__(4 * sizeof(__bf16))));
-typedef __attribute__((address_space(3))) bf16x4 lds_bf16x4;
 
 __device__ inline u32x4 load16(const u16* p) { return *reinterpret_cast<const u32x4*>(p); }
 
@@ -144,6 +177,43 @@ __device__ inline float other_half(float x) {
   const auto sw = __builtin_amdgcn_permlane32_swap(u, u, false, false);
   const unsigned lane = __builtin_amdgcn_mbcnt_hi(~0u, __builtin_amdgcn_mbcnt_lo(~0u, 0u));
   return __builtin_bit_cast(float, lane < 32 ? sw[1] : sw[0]);
+}
+
+// LDS byte address of a pointer into a __shared__ array.
+__device__ inline uint32_t lds_addr(const void* p) {
+  return static_cast<uint32_t>(reinterpret_cast<size_t>((const lds_void*)p));
+}
+
+// ds_read_b64_tr_b16 at a VGPR address plus a constant byte offset.  Within
+// each 16-lane group, lane 4r + c supplies the address of four consecutive
+// 16-bit elements of row r (c = 0..3) and receives element c of each of the
+// four rows.  Issued as inline assembly: the compiler's builtin for this
+// instruction makes it wait for every outstanding HBM-to-LDS load first,
+// including the prefetch of the next tile, which it cannot tell apart from
+// the tile being read.  The results are therefore not tracked by the
+// compiler; lds_wait<N>() followed by lds_bind() on each result makes them
+// usable once at most N LDS operations of this wave are still outstanding
+// (LDS operations complete in order).
+template <int kOff>
+__device__ inline u32x2 lds_read_tr16(uint32_t addr) {
+  u32x2 r;
+  asm volatile("ds_read_b64_tr_b16 %0, %1 offset:%2" : "=v"(r) : "v"(addr), "i"(kOff) : "memory");
+  return r;
+}
+template <int N>
+__device__ inline void lds_wait() {
+  asm volatile("s_waitcnt lgkmcnt(%0)" ::"i"(N) : "memory");
+}
+__device__ inline void lds_bind(u32x2& r) { asm volatile("" : "+v"(r)); }
+
+// Calls f(std::integral_constant<int, I>) for I = 0 .. N-1, so that the index
+// can form a constant operand.
+template <int I, int N, typename F>
+__device__ inline void static_for(F&& f) {
+  if constexpr (I < N) {
+    f(std::integral_constant<int, I>{});
+    static_for<I + 1, N>(f);
+  }
 }
 
 // Word 3 of a raw buffer resource on gfx9-family GPUs (32-bit data format,
@@ -265,6 +335,12 @@ __global__ __launch_bounds__(kThreads) void attn_fwd_bf16(AttnArgs a) {
   // columns 4cb..4cb+3, and receives one column across the four rows.
   const int tr_r = (lane & 15) >> 2;
   const int tr_d = ((lane >> 4) & 1) * 16 + (lane & 3) * 4;
+  int vtr_off[DB];  // byte offset of this lane's address in key rows 0..7
+#pragma unroll
+  for (int db = 0; db < DB; ++db) {
+    const int d = db * 32 + tr_d;
+    vtr_off[db] = TL::offset(4 * hi + tr_r, d >> 3) + (d & 7) * 2;
+  }
 
   load_tile(0, 0);
   __builtin_amdgcn_s_waitcnt(kWaitVmcnt0);
@@ -343,26 +419,23 @@ __global__ __launch_bounds__(kThreads) void attn_fwd_bf16(AttnArgs a) {
       // keys are kb*32 + 16kk + 4hi + {0..3} and the same + 8, matching the
       // keys its half-wave holds in S^T.
       float lp[4] = {0.0f, 0.0f, 0.0f, 0.0f};
-#pragma unroll
-      for (int kb = 0; kb < SB; ++kb) {
-        bf16x8 vf[2][DB];
-#pragma unroll
-        for (int kk = 0; kk < 2; ++kk)
-#pragma unroll
-          for (int db = 0; db < DB; ++db) {
-            const int d = db * 32 + tr_d;
-#pragma unroll
-            for (int t = 0; t < 2; ++t) {
-              const int key = kb * 32 + 16 * kk + 8 * t + 4 * hi + tr_r;
-              const bf16x4 h = __builtin_amdgcn_ds_read_tr16_b64_v4bf16(
-                  (lds_bf16x4*)(vl + TL::offset(key, d >> 3) + (d & 7) * 2));
-#pragma unroll
-              for (int e = 0; e < 4; ++e) vf[kk][db][4 * t + e] = h[e];
-            }
-          }
-        __builtin_amdgcn_sched_barrier(0);  // keep the reads ahead of the exps
-#pragma unroll
-        for (int kk = 0; kk < 2; ++kk) {
+      const uint32_t vaddr = lds_addr(vl);
+      static_for<0, SB>([&](auto KB) {
+        constexpr int kb = decltype(KB)::value;
+        // vf[kk][db][t]: V^T elements of head-dim block db for keys
+        // kb*32 + 16kk + 8t + 4hi + {0..3} (half t of MFMA step kk's A operand).
+        u32x2 vf[2][DB][2];
+        static_for<0, 2>([&](auto KK) {
+          static_for<0, DB>([&](auto DBI) {
+            static_for<0, 2>([&](auto T) {
+              constexpr int kk = decltype(KK)::value, db = decltype(DBI)::value, t = decltype(T)::value;
+              constexpr int row = kb * 32 + 16 * kk + 8 * t;  // multiple of 8: same swizzle as row 0..7
+              vf[kk][db][t] = lds_read_tr16<row * TL::kRowBytes>(vaddr + vtr_off[db]);
+            });
+          });
+        });
+        static_for<0, 2>([&](auto KK) {
+          constexpr int kk = decltype(KK)::value;
           bf16x8 pb;
 #pragma unroll
           for (int e = 0; e < 8; ++e) {
@@ -370,11 +443,17 @@ __global__ __launch_bounds__(kThreads) void attn_fwd_bf16(AttnArgs a) {
             lp[e & 3] += pe;
             pb[e] = (__bf16)pe;
           }
+          lds_wait<(1 - kk) * 2 * DB>();  // step kk's reads done, the later step's may be pending
 #pragma unroll
-          for (int db = 0; db < DB; ++db)
-            acc_o[db] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(vf[kk][db], pb, acc_o[db], 0, 0, 0);
-        }
-      }
+          for (int db = 0; db < DB; ++db) {
+            lds_bind(vf[kk][db][0]);
+            lds_bind(vf[kk][db][1]);
+            const u32x4 a4 = {vf[kk][db][0][0], vf[kk][db][0][1], vf[kk][db][1][0], vf[kk][db][1][1]};
+            acc_o[db] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(__builtin_bit_cast(bf16x8, a4), pb,
+                                                                acc_o[db], 0, 0, 0);
+          }
+        });
+      });
       l_run += (lp[0] + lp[1]) + (lp[2] + lp[3]);
     }
     // The next tile's loads have landed in LDS and every wave is done with
@@ -523,7 +602,10 @@ hipError_t launch_attention(const Plan& plan, const void* q, const void* k, cons
     } else {
       pa = PatArgs{1, 1, 1, 1, 1, 0, 0, 0};
     }
+    a.order[i] = static_cast<int8_t>(i);
   }
+  std::stable_sort(a.order, a.order + plan.npat,
+                   [&](int8_t x, int8_t y) { return plan.pat[x].ntiles > plan.pat[y].ntiles; });
   if (plan.total_items == 0) return hipSuccess;
   // XCD 0 holds the most units of every pattern; the launch covers 8 times its slots.
   const dim3 grid(static_cast<unsigned>(plan.launch_items));
