@@ -5,9 +5,13 @@ the N=32768, H=12, D=64 bf16 workload with the five patterns
 (2048,1) (4096,2) (8192,4) (16384,6) (32768,12), inputs resident in HBM.
 
 Prints one JSON line: effective TFLOP/s over the exact sparse flops (4*D per
-unmasked query-key pair), tokens/s, per-stage times measured with HIP events
-recorded by the library on the call's stream, the attention stage's MFMA
+unmasked query-key pair) and tokens/s of the timed back-to-back steps, per-stage
+times from a second pass in which the library records HIP events around each
+of its kernels on the call's stream, the attention stage's MFMA
 roofline fraction, and the CPU oracle timed on a bounded sample on this host.
+After the timed region, a second pass times each step on its own (median,
+minimum, mean), once as is and once with a 512 MiB buffer written before each
+step so that the inputs are no longer held in the Infinity Cache.
 """
 from __future__ import annotations
 
@@ -36,6 +40,8 @@ def parse():
     ap.add_argument("--workload", default=DEFAULT_WORKLOAD)
     ap.add_argument("--cpu-seconds", type=float, default=12.0,
                     help="minimum CPU time spent on the oracle sample (0 skips the CPU baseline)")
+    ap.add_argument("--dist-steps", type=int, default=20,
+                    help="steps of the per-step pass (unflushed and flushed each); 0 skips it")
     ap.add_argument("--copy-calibration-mib", type=int, default=0,
                     help="only run a plain device-to-device copy of this many MiB (5 times), to "
                          "calibrate the HBM byte counters of a profiler against a known size")
@@ -53,23 +59,58 @@ def copy_calibration(mib):
     print(json.dumps({"copy_calibration_bytes_each_way": mib * (1 << 20), "launches": 5}), flush=True)
 
 
-def profiled_traffic(workload):
-    """HBM bytes per launch of the attention and combine kernels measured with
-    rocprofv3 FETCH_SIZE / WRITE_SIZE (scaled by a plain copy of known size),
-    or None when the attention kernel's source changed since the measurement."""
+def profiled_counters(workload):
+    """Per-launch figures measured with rocprofv3 counters for the current
+    attention source: HBM bytes of the attention and combine kernels
+    (FETCH_SIZE / WRITE_SIZE scaled by a plain copy of known size) and the
+    attention kernel's MFMA busy percentage.  Empty when the attention kernel's
+    source changed since the measurement."""
     import hashlib
     if not os.path.exists(PROFILED_TRAFFIC):
-        return None, None
+        return {}
     with open(PROFILED_TRAFFIC) as f:
         rec = json.load(f).get(workload)
     if not rec:
-        return None, None
+        return {}
     src = os.path.join(ROOT, "paper_2307_02486_amd", "csrc", "attn_fwd.hip")
     with open(src, "rb") as f:
         sha = hashlib.sha256(f.read()).hexdigest()[:16]
     if sha != rec.get("attn_fwd_hip_sha256_16"):
-        return None, None
-    return rec.get("attention_bytes_per_launch"), rec.get("combine_bytes_per_launch")
+        return {}
+    return rec
+
+
+def step_distribution(step, stream, steps, flush_bytes):
+    """Times `steps` single steps with events around each one; with
+    flush_bytes > 0 a buffer of that size is written before every step."""
+    import statistics
+
+    import torch
+    scratch = torch.empty(flush_bytes // 4, dtype=torch.float32, device=stream.device) if flush_bytes else None
+    times = []
+    for i in range(steps):
+        if scratch is not None:
+            scratch.fill_(float(i))
+        e0 = torch.cuda.Event(enable_timing=True)
+        e1 = torch.cuda.Event(enable_timing=True)
+        e0.record(stream)
+        step()
+        e1.record(stream)
+        e1.synchronize()
+        times.append(e0.elapsed_time(e1))
+    return {"median_ms": round(statistics.median(times), 5), "min_ms": round(min(times), 5),
+            "mean_ms": round(statistics.fmean(times), 5), "steps": steps}
+
+
+def cpu_model():
+    try:
+        with open("/proc/cpuinfo") as f:
+            for line in f:
+                if line.startswith("model name"):
+                    return line.split(":", 1)[1].strip()
+    except OSError:
+        pass
+    return "unknown"
 
 
 def cpu_baseline(wl, q, k, v, min_seconds):
@@ -107,6 +148,7 @@ def cpu_baseline(wl, q, k, v, min_seconds):
                   f"({blas}), {dt:.1f} s",
         "tokens_per_s": wl.B * wl.N * len(done) / wl.H / dt,
         "host_cpus": len(os.sched_getaffinity(0)),
+        "cpu_model": cpu_model(),
     }
 
 
@@ -146,15 +188,21 @@ def main():
     torch.cuda.synchronize()
     t_start = torch.cuda.Event(enable_timing=True)
     t_end = torch.cuda.Event(enable_timing=True)
-    with StageTimer(capacity=max(1, args.steps)) as st:
-        torch.cuda.synchronize()
-        t_start.record(stream)
-        for _ in range(args.steps):
-            step()
-        t_end.record(stream)
-        torch.cuda.synchronize()
+    # Timed region: exactly `steps` back-to-back calls, nothing else on the stream.
+    torch.cuda.synchronize()
+    t_start.record(stream)
+    for _ in range(args.steps):
+        step()
+    t_end.record(stream)
+    torch.cuda.synchronize()
     total_ms = t_start.elapsed_time(t_end)
     ms = total_ms / args.steps
+    # Per-stage split: the same number of calls again, with the library recording
+    # HIP events around each of its two kernels on the call's stream.
+    with StageTimer(capacity=max(1, args.steps)) as st:
+        for _ in range(args.steps):
+            step()
+        torch.cuda.synchronize()
     ms_attn = st.ms_attention / max(1, st.calls)
     ms_comb = st.ms_combine / max(1, st.calls)
     flops = info["sparse_flops"]
@@ -162,7 +210,9 @@ def main():
     attn_tflops = flops / (ms_attn * 1e-3) / 1e12
     comb_gbs = info["bytes_combine"] / (ms_comb * 1e-3) / 1e9
     peak = PEAK_BF16_TFLOPS if wl.dtype == "bf16" else PEAK_F32_TFLOPS
-    traffic, comb_traffic = profiled_traffic(wl.name)
+    prof = profiled_counters(wl.name)
+    traffic = prof.get("attention_bytes_per_launch")
+    comb_traffic = prof.get("combine_bytes_per_launch")
     res = {
         "metric": METRIC,
         "value": round(tflops, 3),
@@ -180,7 +230,8 @@ def main():
         "tokens_per_s": round(wl.B * wl.N / (ms * 1e-3), 1),
         "sparse_flops": flops,
         "attention_stage": {"ms": round(ms_attn, 5), "tflops": round(attn_tflops, 3),
-                            "frac_of_mfma_peak": round(attn_tflops / peak, 4)},
+                            "frac_of_mfma_peak": round(attn_tflops / peak, 4),
+                            "mfma_busy_pct_profiled": prof.get("attention_mfma_busy_pct")},
         "combine_stage": {"ms": round(ms_comb, 5), "algorithmic_bytes": info["bytes_combine"],
                           "gbps": round(comb_gbs, 1), "frac_of_hbm_peak": round(comb_gbs / PEAK_HBM_GBS, 4),
                           "traffic": comb_traffic},
@@ -188,6 +239,11 @@ def main():
                      "unit": "TFLOP/s", "frac": round(attn_tflops / peak, 4), "traffic": traffic},
         "cpu_baseline": None,
     }
+    if args.dist_steps > 0:
+        res["step_distribution"] = {
+            "unflushed": step_distribution(step, stream, args.dist_steps, 0),
+            "flushed_512MiB": step_distribution(step, stream, args.dist_steps, 512 << 20),
+        }
     if args.cpu_seconds > 0:
         res["cpu_baseline"] = cpu_baseline(wl, q, k, v, args.cpu_seconds)
     print(json.dumps(res), flush=True)
