@@ -50,8 +50,9 @@ struct AttnArgs {
   char* ws;
   int32_t B, N, H, npat, causal, total_items;
   float scale_log2;  // softmax scale times log2(e): scores go to exp2 directly
+  // The patterns, ordered by query tiles per unit, most first (the kernels
+  // only use a pattern's index to find its record here).
   PatArgs pat[DA_MAX_PATTERNS];
-  int8_t order[DA_MAX_PATTERNS];  // patterns by query tiles per unit, most first
 };
 
 // One attention work item: which segment of which pattern, and which query tile.
@@ -69,8 +70,8 @@ struct Item {
 // so launch index x is mapped to XCD c = x mod 8 and the units with index = c
 // (mod 8) are given to that XCD: the query tiles of one segment run on one
 // XCD and its K/V rows are fetched into that XCD's L2 once.  On each XCD the
-// items come in two phases.  First, pattern by pattern (those with the most
-// query tiles per segment first) and unit by unit, the query tiles from the
+// items come in two phases.  First, pattern by pattern (in the order of the
+// records, those with the most query tiles per segment first) and unit by unit, the query tiles from the
 // last (the longest under a causal mask) down to tile kShortTiles, so the
 // tiles of a segment run close together in time.  Then
 // the first kShortTiles query tiles of every unit, level by level from tile
@@ -87,8 +88,11 @@ __device__ inline bool decode_item(const AttnArgs& a, int bid, int block_m, Item
   const int c = bid & 7;
   int slot = bid >> 3;
   int pi = -1, j = 0, tq = 0;
-  for (int o = 0; o < a.npat; ++o) {
-    const int p = a.order[o];
+  // Fully unrolled: the records are read with constant offsets, in a few
+  // scalar loads issued together.
+#pragma unroll
+  for (int p = 0; p < DA_MAX_PATTERNS; ++p) {
+    if (p >= a.npat) break;
     const PatArgs& P = a.pat[p];
     const int nlong = P.ntiles > kShortTiles ? P.ntiles - kShortTiles : 0;
     const int n = units_on_xcd(P, c) * nlong;
@@ -100,8 +104,12 @@ __device__ inline bool decode_item(const AttnArgs& a, int bid, int block_m, Item
     }
     slot -= n;
   }
-  for (int t = kShortTiles - 1; pi < 0 && t >= 0; --t) {
-    for (int p = 0; p < a.npat; ++p) {
+#pragma unroll
+  for (int t = kShortTiles - 1; t >= 0; --t) {
+    if (pi >= 0) break;
+#pragma unroll
+    for (int p = 0; p < DA_MAX_PATTERNS; ++p) {
+      if (p >= a.npat) break;
       const PatArgs& P = a.pat[p];
       const int n = P.ntiles > t ? units_on_xcd(P, c) : 0;
       if (slot < n) {
@@ -253,21 +261,17 @@ __global__ __launch_bounds__(kThreads) void attn_fwd_bf16(AttnArgs a) {
   const bool q_valid = tq_row < L;
   const int64_t row_step = it.rstride * D;  // elements between consecutive kept rows
 
-  // Q^T operand: lane holds query tq_row, head-dim slice [16c + 8hi, +8),
-  // multiplied by scale * log2(e) and rounded to bf16: the MFMA then yields
-  // scores in log2 units and the exponent needs no per-score multiply.
-  bf16x8 qreg[KC];
+  // Q^T operand: lane holds query tq_row, head-dim slice [16c + 8hi, +8).  The
+  // loads are issued here and consumed after the first K/V tile's loads have
+  // been issued, so the two latencies overlap.
+  // Rows past the segment's end load its last row (unconditional loads, no
+  // branches) and are zeroed at the conversion.
+  u32x4 qraw[KC];
   {
-    const u16* qp = qg + (it.row0 + (int64_t)tq_row * it.rstride) * D + 8 * hi;
+    const int qrow = min(tq_row, L - 1);
+    const u16* qp = qg + (it.row0 + (int64_t)qrow * it.rstride) * D + 8 * hi;
 #pragma unroll
-    for (int c = 0; c < KC; ++c) {
-      u32x4 x = q_valid ? load16(qp + 16 * c) : u32x4{0, 0, 0, 0};
-#pragma unroll
-      for (int e = 0; e < 8; ++e) {
-        const unsigned bits = (x[e >> 1] >> (16 * (e & 1))) << 16;
-        qreg[c][e] = (__bf16)(__builtin_bit_cast(float, bits) * a.scale_log2);
-      }
-    }
+    for (int c = 0; c < KC; ++c) qraw[c] = load16(qp + 16 * c);
   }
 
   // Tile loads go straight from HBM to LDS (no registers, no LDS stores).
@@ -343,6 +347,16 @@ __global__ __launch_bounds__(kThreads) void attn_fwd_bf16(AttnArgs a) {
   }
 
   load_tile(0, 0);
+  // Q multiplied by scale * log2(e) and rounded to bf16: the MFMA then yields
+  // scores in log2 units and the exponent needs no per-score multiply.
+  bf16x8 qreg[KC];
+#pragma unroll
+  for (int c = 0; c < KC; ++c)
+#pragma unroll
+    for (int e = 0; e < 8; ++e) {
+      const unsigned bits = q_valid ? (qraw[c][e >> 1] >> (16 * (e & 1))) << 16 : 0u;
+      qreg[c][e] = (__bf16)(__builtin_bit_cast(float, bits) * a.scale_log2);
+    }
   __builtin_amdgcn_s_waitcnt(kWaitVmcnt0);
   __syncthreads();
   for (int jt = 0; jt < ntile; ++jt) {
@@ -587,10 +601,14 @@ hipError_t launch_attention(const Plan& plan, const void* q, const void* k, cons
   a.causal = plan.causal;
   a.total_items = static_cast<int32_t>(plan.total_items);
   a.scale_log2 = plan.scale * kLog2e;
+  int order[DA_MAX_PATTERNS];
+  for (int i = 0; i < plan.npat; ++i) order[i] = i;
+  std::stable_sort(order, order + plan.npat,
+                   [&](int x, int y) { return plan.pat[x].ntiles > plan.pat[y].ntiles; });
   for (int i = 0; i < DA_MAX_PATTERNS; ++i) {
     PatArgs& pa = a.pat[i];
     if (i < plan.npat) {
-      const PatternPlan& pp = plan.pat[i];
+      const PatternPlan& pp = plan.pat[order[i]];
       pa.w = static_cast<int32_t>(pp.w);
       pa.r = static_cast<int32_t>(pp.r);
       pa.nseg = static_cast<int32_t>(pp.nseg);
@@ -602,10 +620,7 @@ hipError_t launch_attention(const Plan& plan, const void* q, const void* k, cons
     } else {
       pa = PatArgs{1, 1, 1, 1, 1, 0, 0, 0};
     }
-    a.order[i] = static_cast<int8_t>(i);
   }
-  std::stable_sort(a.order, a.order + plan.npat,
-                   [&](int8_t x, int8_t y) { return plan.pat[x].ntiles > plan.pat[y].ntiles; });
   if (plan.total_items == 0) return hipSuccess;
   // XCD 0 holds the most units of every pattern; the launch covers 8 times its slots.
   const dim3 grid(static_cast<unsigned>(plan.launch_items));
