@@ -51,9 +51,11 @@ template <typename WsT> struct Vec8;
 template <> struct Vec8<_Float16> { typedef f16x8 type; };
 template <> struct Vec8<float> { typedef f32x8 type; };
 
+// Workspace rows and lse values are read exactly once: nontemporal loads.
 template <typename WsT>
 __device__ inline typename Vec8<WsT>::type load8(const WsT* p) {
-  return *reinterpret_cast<const typename Vec8<WsT>::type*>(p);
+  typedef typename Vec8<WsT>::type V;
+  return __builtin_nontemporal_load(reinterpret_cast<const V*>(p));
 }
 
 __device__ inline f32x8 to_f32(const f16x8& h) {
@@ -64,74 +66,94 @@ __device__ inline f32x8 to_f32(const f16x8& h) {
 }
 __device__ inline f32x8 to_f32(const f32x8& v) { return v; }
 
+// out and lse are written once and not read again by this call: nontemporal stores.
 __device__ inline void store8(float* p, const f32x8& v) {
-  *reinterpret_cast<f32x4*>(p) = f32x4{v[0], v[1], v[2], v[3]};
-  *reinterpret_cast<f32x4*>(p + 4) = f32x4{v[4], v[5], v[6], v[7]};
+  __builtin_nontemporal_store(f32x4{v[0], v[1], v[2], v[3]}, reinterpret_cast<f32x4*>(p));
+  __builtin_nontemporal_store(f32x4{v[4], v[5], v[6], v[7]}, reinterpret_cast<f32x4*>(p + 4));
 }
 
 __device__ inline void store8(unsigned short* p, const f32x8& v) {
   bf16x8 b;
 #pragma unroll
   for (int e = 0; e < 8; ++e) b[e] = (__bf16)v[e];
-  *reinterpret_cast<bf16x8*>(p) = b;
+  __builtin_nontemporal_store(b, reinterpret_cast<bf16x8*>(p));
 }
 
-template <int D, typename OutT, typename WsT>
+// Each lane owns eight head-dim elements of kRows rows; a workgroup covers
+// kRows * RPB consecutive positions (RPB = threads / lanes per row), and a
+// lane's rows are RPB positions apart.  NP >= npat bounds the pattern loop at
+// compile time, so that only NP sets of registers are held per row.
+constexpr int kRows = 1;  // rows per lane (two measured slower: fewer waves resident)
+
+template <int D, typename OutT, typename WsT, int NP>
 __global__ __launch_bounds__(kThreads) void combine_fwd(CombArgs a) {
   constexpr int LPR = D / 8;            // lanes per row
-  constexpr int RPB = kThreads / LPR;   // rows per workgroup
+  constexpr int RPB = kThreads / LPR;   // rows per workgroup and pass
   const int tid = __builtin_amdgcn_workitem_id_x();
   const int blk = __builtin_amdgcn_workgroup_id_x();
   const int bh = blk / a.chunks;
-  const int p = (blk - bh * a.chunks) * RPB + tid / LPR;
+  const int p0 = (blk - bh * a.chunks) * (RPB * kRows) + tid / LPR;
   const int d0 = (tid % LPR) * 8;
-  if (p >= a.N) return;
   const int h = bh % a.H;
+  const int b = bh / a.H;
 
-  // Issue the loads of every pattern that keeps this row.
-  typename Vec8<WsT>::type o[DA_MAX_PATTERNS];
-  float li[DA_MAX_PATTERNS];
+  // Issue the loads of every pattern that keeps each of this lane's rows.
+  typename Vec8<WsT>::type o[kRows][NP];
+  float li[kRows][NP];
 #pragma unroll
-  for (int i = 0; i < DA_MAX_PATTERNS; ++i) {
-    li[i] = -INFINITY;
-    if (i >= a.npat) continue;
-    const CombPat& P = a.pat[i];
-    const uint32_t g = P.fw.div(static_cast<uint32_t>(p));
-    const uint32_t pos = static_cast<uint32_t>(p) - g * P.fw.d;
-    const uint32_t t = P.fr.div(pos);
-    const uint32_t s = static_cast<uint32_t>(h) - P.fr.div(static_cast<uint32_t>(h)) * P.fr.d;
-    if (pos - t * P.fr.d != s) continue;
-    const int64_t row = ((int64_t)bh * P.nseg + g) * P.lmax + t;
-    li[i] = reinterpret_cast<const float*>(a.ws + P.lse_off)[row];
-    o[i] = load8(reinterpret_cast<const WsT*>(a.ws + P.o_off) + row * D + d0);
+  for (int k = 0; k < kRows; ++k) {
+    const int p = p0 + k * RPB;
+#pragma unroll
+    for (int i = 0; i < NP; ++i) {
+      li[k][i] = -INFINITY;
+      if (i >= a.npat || p >= a.N) continue;
+      const CombPat& P = a.pat[i];
+      const uint32_t g = P.fw.div(static_cast<uint32_t>(p));
+      const uint32_t pos = static_cast<uint32_t>(p) - g * P.fw.d;
+      const uint32_t t = P.fr.div(pos);
+      const uint32_t s = static_cast<uint32_t>(h) - P.fr.div(static_cast<uint32_t>(h)) * P.fr.d;
+      if (pos - t * P.fr.d != s) continue;
+      const int64_t row = ((int64_t)bh * P.nseg + g) * P.lmax + t;
+      li[k][i] = __builtin_nontemporal_load(reinterpret_cast<const float*>(a.ws + P.lse_off) + row);
+      o[k][i] = load8(reinterpret_cast<const WsT*>(a.ws + P.o_off) + row * D + d0);
+    }
   }
   // Combined log-sum-exp, then the denominator-weighted sum.
-  float m = -INFINITY;
 #pragma unroll
-  for (int i = 0; i < DA_MAX_PATTERNS; ++i) m = fmaxf(m, li[i]);
-  const int b = bh / a.H;
-  OutT* out = static_cast<OutT*>(a.out) + (((int64_t)b * a.N + p) * a.H + h) * D + d0;
-  float lse_v = -INFINITY;
-  f32x8 acc = f32x8{0, 0, 0, 0, 0, 0, 0, 0};
-  if (m != -INFINITY) {
-    float den = 0.0f;
+  for (int k = 0; k < kRows; ++k) {
+    const int p = p0 + k * RPB;
+    if (p >= a.N) continue;
+    float m = -INFINITY;
 #pragma unroll
-    for (int i = 0; i < DA_MAX_PATTERNS; ++i) {
-      if (li[i] == -INFINITY) continue;
-      const float e = __builtin_amdgcn_exp2f((li[i] - m) * kLog2e);
-      den += e;
-      acc += e * to_f32(o[i]);
+    for (int i = 0; i < NP; ++i) m = fmaxf(m, li[k][i]);
+    OutT* out = static_cast<OutT*>(a.out) + (((int64_t)b * a.N + p) * a.H + h) * D + d0;
+    float lse_v = -INFINITY;
+    f32x8 acc = f32x8{0, 0, 0, 0, 0, 0, 0, 0};
+    if (m != -INFINITY) {
+      float den = 0.0f;
+#pragma unroll
+      for (int i = 0; i < NP; ++i) {
+        if (li[k][i] == -INFINITY) continue;
+        const float e = __builtin_amdgcn_exp2f((li[k][i] - m) * kLog2e);
+        den += e;
+        acc += e * to_f32(o[k][i]);
+      }
+      acc *= 1.0f / den;
+      lse_v = m + __builtin_amdgcn_logf(den) * kLn2;
     }
-    acc *= 1.0f / den;
-    lse_v = m + __builtin_amdgcn_logf(den) * kLn2;
+    store8(out, acc);
+    if (d0 == 0) __builtin_nontemporal_store(lse_v, a.lse + (int64_t)bh * a.N + p);
   }
-  store8(out, acc);
-  if (d0 == 0) a.lse[(int64_t)bh * a.N + p] = lse_v;
 }
 
 template <int D, typename OutT, typename WsT>
 void launch_one(const dim3& grid, hipStream_t stream, const CombArgs& a) {
-  hipLaunchKernelGGL((combine_fwd<D, OutT, WsT>), grid, dim3(kThreads), 0, stream, a);
+  if (a.npat <= 4)
+    hipLaunchKernelGGL((combine_fwd<D, OutT, WsT, 4>), grid, dim3(kThreads), 0, stream, a);
+  else if (a.npat <= 8)
+    hipLaunchKernelGGL((combine_fwd<D, OutT, WsT, 8>), grid, dim3(kThreads), 0, stream, a);
+  else
+    hipLaunchKernelGGL((combine_fwd<D, OutT, WsT, DA_MAX_PATTERNS>), grid, dim3(kThreads), 0, stream, a);
 }
 
 }  // namespace
@@ -159,8 +181,8 @@ hipError_t launch_combine(const Plan& plan, const void* workspace, void* out, fl
       c = CombPat{make_fastdiv(1), make_fastdiv(1), 1, 1, 0, 0};
     }
   }
-  const int rpb = kThreads / (static_cast<int>(plan.D) / 8);
-  a.chunks = static_cast<int32_t>((plan.N + rpb - 1) / rpb);
+  const int rows = kThreads / (static_cast<int>(plan.D) / 8) * kRows;  // positions per workgroup
+  a.chunks = static_cast<int32_t>((plan.N + rows - 1) / rows);
   const int64_t blocks = static_cast<int64_t>(a.chunks) * plan.B * plan.H;
   if (blocks >= (int64_t{1} << 31)) return hipErrorInvalidValue;
   const dim3 grid(static_cast<unsigned>(blocks));
