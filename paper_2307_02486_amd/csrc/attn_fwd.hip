@@ -156,16 +156,26 @@ constexpr float kRescaleSlack = 8.0f;
 
 // K and V tiles live in LDS row-major (kBN rows of D bf16), without padding:
 // a row is D/8 16-byte slots and logical slot c of row k is stored at slot
-// c ^ (k & swz), so eight consecutive rows read at one logical slot hit eight
-// different bank groups.
+// c ^ swz(k).  LDS serves 256 bytes per cycle from 64 four-byte banks, i.e.
+// sixteen 16-byte bank groups; a 16-byte read is served 16 lanes per cycle,
+// an 8-byte read 32 lanes per cycle.  swz(k) makes both access patterns of
+// the kernel conflict-free:
+//   K fragments: 16 consecutive rows at one logical slot -> 16 bank groups;
+//   V^T reads:   4 consecutive rows (aligned) x 4 consecutive slots -> 16.
+// Row k starts at bank group (k * D/8) mod 16, which swz(k) complements; it
+// depends on bits 0-3 of k only, so rows 16 apart share it.
 template <int D>
 struct TileLayout {
   static constexpr int kSlots = D / 8;                     // 16-byte slots per row
-  static constexpr int kSwz = kSlots < 8 ? kSlots - 1 : 7; // swizzle mask
   static constexpr int kRowBytes = D * 2;
   static constexpr int kTileBytes = kBN * kRowBytes;
+  __device__ static int swz(int row) {
+    if constexpr (D == 32) return (row >> 2) & 3;
+    else if constexpr (D == 64) return (((row >> 1) & 1) << 2) | ((row >> 2) & 3);
+    else return ((row & 3) << 2) | ((row >> 2) & 3);
+  }
   __device__ static int offset(int row, int slot) {        // byte offset of a slot
-    return row * kRowBytes + ((slot ^ (row & kSwz)) << 4);
+    return row * kRowBytes + ((slot ^ swz(row)) << 4);
   }
 };
 
@@ -283,7 +293,7 @@ __global__ __launch_bounds__(kThreads) void attn_fwd_bf16(AttnArgs a) {
   for (int i = 0; i < kLoadsPerWave; ++i) {
     const int s = 64 * (wv * kLoadsPerWave + i) + lane;
     lrow[i] = s / TL::kSlots;
-    lslot[i] = (s % TL::kSlots) ^ (lrow[i] & TL::kSwz);
+    lslot[i] = (s % TL::kSlots) ^ TL::swz(lrow[i]);
   }
   const u16* kbase = static_cast<const u16*>(a.k) + it.row0 * D;
   const u16* vbase = static_cast<const u16*>(a.v) + it.row0 * D;
@@ -339,12 +349,14 @@ __global__ __launch_bounds__(kThreads) void attn_fwd_bf16(AttnArgs a) {
   // columns 4cb..4cb+3, and receives one column across the four rows.
   const int tr_r = (lane & 15) >> 2;
   const int tr_d = ((lane >> 4) & 1) * 16 + (lane & 3) * 4;
-  int vtr_off[DB];  // byte offset of this lane's address in key rows 0..7
+  int vtr_off[DB][2];  // byte offset of this lane's address in key rows 0..15
 #pragma unroll
-  for (int db = 0; db < DB; ++db) {
-    const int d = db * 32 + tr_d;
-    vtr_off[db] = TL::offset(4 * hi + tr_r, d >> 3) + (d & 7) * 2;
-  }
+  for (int db = 0; db < DB; ++db)
+#pragma unroll
+    for (int t = 0; t < 2; ++t) {
+      const int d = db * 32 + tr_d;
+      vtr_off[db][t] = TL::offset(8 * t + 4 * hi + tr_r, d >> 3) + (d & 7) * 2;
+    }
 
   load_tile(0, 0);
   // Q multiplied by scale * log2(e) and rounded to bf16: the MFMA then yields
@@ -443,8 +455,8 @@ __global__ __launch_bounds__(kThreads) void attn_fwd_bf16(AttnArgs a) {
           static_for<0, DB>([&](auto DBI) {
             static_for<0, 2>([&](auto T) {
               constexpr int kk = decltype(KK)::value, db = decltype(DBI)::value, t = decltype(T)::value;
-              constexpr int row = kb * 32 + 16 * kk + 8 * t;  // multiple of 8: same swizzle as row 0..7
-              vf[kk][db][t] = lds_read_tr16<row * TL::kRowBytes>(vaddr + vtr_off[db]);
+              constexpr int row = kb * 32 + 16 * kk;  // multiple of 16: same swizzle as rows 0..15
+              vf[kk][db][t] = lds_read_tr16<row * TL::kRowBytes>(vaddr + vtr_off[db][t]);
             });
           });
         });
