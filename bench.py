@@ -42,6 +42,9 @@ def parse():
                     help="minimum CPU time spent on the oracle sample (0 skips the CPU baseline)")
     ap.add_argument("--dist-steps", type=int, default=20,
                     help="steps of the per-step pass (unflushed and flushed each); 0 skips it")
+    ap.add_argument("--sweep", action="store_true",
+                    help="instead of the benchmark: the dense-versus-dilated sweep over N = 8K..1M "
+                         "(fixed tokens per batch), one JSON line per (N, variant)")
     ap.add_argument("--copy-calibration-mib", type=int, default=0,
                     help="only run a plain device-to-device copy of this many MiB (5 times), to "
                          "calibrate the HBM byte counters of a profiler against a known size")
@@ -152,6 +155,52 @@ def cpu_baseline(wl, q, k, v, min_seconds):
     }
 
 
+def sweep(args):
+    """Dense (w = N, r = 1) and dilated ({(2048, 1), (N, N/2048)}) forward
+    passes at a fixed 2^20 tokens per batch for N = 8K .. 1M; per (N, variant)
+    the median of `steps` timed calls (events on the call's stream) after
+    `warmup` calls."""
+    import statistics
+
+    import torch
+
+    import workloads
+    from paper_2307_02486_amd import dilated_attn, plan, workspace_for
+    dev = torch.device("cuda:0")
+    torch.cuda.set_device(dev)
+    stream = torch.cuda.current_stream(dev)
+    steps, warm = max(1, min(args.steps, 5)), max(1, min(args.warmup, 2))
+    for N in workloads.SWEEP_N:
+        for variant in ("dense", "dilated"):
+            wl = workloads.sweep_workload(N, variant)
+            q, k, v = workloads.make_qkv(wl, device=dev)
+            pats = list(wl.patterns)
+            info = plan(wl.B, wl.N, wl.H, wl.D, pats, wl.causal, wl.torch_dtype)
+            out = torch.empty_like(q)
+            lse = torch.empty((wl.B, wl.H, wl.N), dtype=torch.float32, device=dev)
+            ws = workspace_for(q, pats, wl.causal)
+            for _ in range(warm):
+                dilated_attn(q, k, v, pats, wl.causal, out=out, lse=lse, workspace=ws, stream=stream)
+            times = []
+            for _ in range(steps):
+                e0 = torch.cuda.Event(enable_timing=True)
+                e1 = torch.cuda.Event(enable_timing=True)
+                e0.record(stream)
+                dilated_attn(q, k, v, pats, wl.causal, out=out, lse=lse, workspace=ws, stream=stream)
+                e1.record(stream)
+                e1.synchronize()
+                times.append(e0.elapsed_time(e1))
+            ms = statistics.median(times)
+            print(json.dumps({"sweep": "dense-vs-dilated", "variant": variant, "N": N, "B": wl.B,
+                              "H": wl.H, "D": wl.D, "dtype": "bf16", "patterns": [list(p) for p in pats],
+                              "median_ms": round(ms, 4), "min_ms": round(min(times), 4), "steps": steps,
+                              "sparse_flops": info["sparse_flops"],
+                              "tflops": round(info["sparse_flops"] / (ms * 1e-3) / 1e12, 2),
+                              "tokens_per_s": round(wl.B * wl.N / (ms * 1e-3), 1)}), flush=True)
+            del q, k, v, out, lse, ws
+            torch.cuda.empty_cache()
+
+
 def main():
     args = parse()
     if args.gpus != 1:
@@ -160,6 +209,9 @@ def main():
         sys.exit(2)
     if args.copy_calibration_mib > 0:
         copy_calibration(args.copy_calibration_mib)
+        return
+    if args.sweep:
+        sweep(args)
         return
     import torch
 

@@ -163,3 +163,26 @@ def test_stream_argument():
         o, l = dilated_attn(q, k, v, [(128, 1), (512, 4)], stream=s)
     s.synchronize()
     assert torch.equal(o, ref_o) and torch.equal(l, ref_l)
+
+
+# ---- the dense-versus-dilated sweep's configurations ----------------------------
+
+@pytest.mark.parametrize("variant", ["dense", "dilated"])
+@pytest.mark.parametrize("N", [8192, 131072])
+def test_sweep_config_sampled_rows(N, variant):
+    """The sweep's shapes (2^20 tokens, H=16, D=128): every row finite, and
+    sampled rows of the first and last (b, h) against the oracle."""
+    wl = workloads.sweep_workload(N, variant)
+    note(f"[parity] {wl.name} sampled rows")
+    q, k, v = workloads.make_qkv(wl, device="cuda")
+    out, lse = run_gpu(q, k, v, list(wl.patterns), wl.causal)
+    assert torch.isfinite(lse).all().item()
+    assert torch.isfinite(out).all().item()
+    rng = np.random.default_rng(wl.seed)
+    rows = []
+    for b in sorted({0, wl.B - 1}):
+        for h in sorted({0, wl.H - 1}):
+            ps = set(rng.integers(0, N, 24).tolist()) | {0, 2047, 2048, N - 1}
+            rows += [(b, int(p), h) for p in sorted(ps)]
+    eo, el = compare_rows(q, k, v, out, lse, wl, rows, tag=wl.name)
+    note(f"[parity] {wl.name}: {len(rows)} rows, out err {eo:.3e} lse err {el:.3e}")

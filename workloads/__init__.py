@@ -111,3 +111,33 @@ def make_random(shape, dtype=torch.float32, sigma=1.0, seed=0, device="cpu",
                 tensor_id=0):
     """A seeded N(0, sigma^2) tensor of any shape, rounded to dtype."""
     return _draw(tuple(shape), dtype, sigma, seed, tensor_id, device)
+
+
+# Dense-versus-dilated runtime sweep on one device, shaped like the paper's
+# runtime experiment (Sec. 3.2): tokens per batch held fixed while N grows from
+# 8K, the dense baseline being one pattern (w = N, r = 1), i.e. vanilla causal
+# attention through the same kernels, and the dilated variant using the
+# experiment's segment lengths on one device, 2048 and N, with dilation rates
+# keeping w / r = 2048 (the geometric rule of Sec. 2.2; the experiment does not
+# state its rates).  H and D are those of the 1M-token workload.
+SWEEP_TOKENS = 1 << 20
+SWEEP_N = [8192 << i for i in range(8)]          # 8K .. 1M
+SWEEP_H, SWEEP_D = 16, 128
+
+
+def sweep_configs():
+    """[(N, B, dense_patterns, dilated_patterns)] for the sweep."""
+    out = []
+    for N in SWEEP_N:
+        B = SWEEP_TOKENS // N
+        out.append((N, B, ((N, 1),), ((2048, 1), (N, N // 2048))))
+    return out
+
+
+def sweep_workload(N: int, variant: str) -> Workload:
+    """The sweep's configuration at sequence length N as a Workload
+    (variant "dense" or "dilated")."""
+    _, B, dense, dilated = {c[0]: c for c in sweep_configs()}[N]
+    pats = dense if variant == "dense" else dilated
+    index = 100 + SWEEP_N.index(N)
+    return Workload(f"sweep_{variant}_n{N}", index, B, N, SWEEP_H, SWEEP_D, "bf16", 1.0, pats)
