@@ -69,7 +69,9 @@ struct Item {
 // Workgroups are handed to the eight XCDs round-robin (launch index mod 8),
 // so launch index x is mapped to XCD c = x mod 8 and the units with index = c
 // (mod 8) are given to that XCD: the query tiles of one segment run on one
-// XCD and its K/V rows are fetched into that XCD's L2 once.  On each XCD the
+// XCD and its K/V rows are fetched into that XCD's L2 once.  (A pattern whose
+// unit count is not a multiple of 8 has its long query tiles dealt to the
+// XCDs one by one instead, trading L2 reuse for balance.)  On each XCD the
 // items come in two phases.  First, pattern by pattern (in the order of the
 // records, those with the most query tiles per segment first) and unit by unit, the query tiles from the
 // last (the longest under a causal mask) down to tile kShortTiles, so the
@@ -87,7 +89,7 @@ __device__ inline int units_on_xcd(const PatArgs& P, int c) {
 __device__ inline bool decode_item(const AttnArgs& a, int bid, int block_m, Item& it) {
   const int c = bid & 7;
   int slot = bid >> 3;
-  int pi = -1, j = 0, tq = 0;
+  int pi = -1, unit = 0, tq = 0;
   // Fully unrolled: the records are read with constant offsets, in a few
   // scalar loads issued together.
 #pragma unroll
@@ -95,14 +97,31 @@ __device__ inline bool decode_item(const AttnArgs& a, int bid, int block_m, Item
     if (p >= a.npat) break;
     const PatArgs& P = a.pat[p];
     const int nlong = P.ntiles > kShortTiles ? P.ntiles - kShortTiles : 0;
-    const int n = units_on_xcd(P, c) * nlong;
-    if (slot < n) {
-      pi = p;
-      j = slot / nlong;
-      tq = P.ntiles - 1 - (slot - j * nlong);
-      break;
+    if ((P.units & 7) == 0) {
+      const int n = units_on_xcd(P, c) * nlong;
+      if (slot < n) {
+        pi = p;
+        const int j = slot / nlong;
+        unit = c + 8 * j;
+        tq = P.ntiles - 1 - (slot - j * nlong);
+        break;
+      }
+      slot -= n;
+    } else {
+      // A unit count that is not a multiple of 8 would load the XCDs
+      // unevenly: the pattern's long items f = unit * nlong + (ntiles-1-tq)
+      // are dealt to the XCDs one by one instead (f = c mod 8 to XCD c).
+      const int total = P.units * nlong;
+      const int n = total > c ? (total - c + 7) >> 3 : 0;
+      if (slot < n) {
+        pi = p;
+        const int f = c + 8 * slot;
+        unit = f / nlong;
+        tq = P.ntiles - 1 - (f - unit * nlong);
+        break;
+      }
+      slot -= n;
     }
-    slot -= n;
   }
 #pragma unroll
   for (int t = kShortTiles - 1; t >= 0; --t) {
@@ -114,7 +133,7 @@ __device__ inline bool decode_item(const AttnArgs& a, int bid, int block_m, Item
       const int n = P.ntiles > t ? units_on_xcd(P, c) : 0;
       if (slot < n) {
         pi = p;
-        j = slot;
+        unit = c + 8 * slot;
         tq = t;
         break;
       }
@@ -123,7 +142,6 @@ __device__ inline bool decode_item(const AttnArgs& a, int bid, int block_m, Item
   }
   if (pi < 0) return false;
   const PatArgs& P = a.pat[pi];
-  const int unit = c + 8 * j;
   it.tq = tq;
   it.pi = pi;
   it.unit = unit;
