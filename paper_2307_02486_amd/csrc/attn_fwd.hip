@@ -506,12 +506,18 @@ __global__ __launch_bounds__(kThreads) void attn_fwd_bf16(AttnArgs a) {
     __syncthreads();
   }
 
-  // Epilogue: normalise and write this lane's row of the per-pattern output.
+  // Epilogue: normalise this wave's 32 rows of the per-pattern output and
+  // stage them in a private LDS region (the tiles are no longer read: the
+  // loop ended with a barrier), so that the stores write whole rows, 16
+  // bytes per lane.  Staged 16-byte chunk x of row k sits at chunk
+  // x ^ ((k >> 1) mod D/8): the 8-byte writes (one row per lane) then hit at
+  // most two lanes per bank pair and the 16-byte reads none.
   const float l_tot = l_run + other_half(l_run);
-  if (!q_valid) return;
   const float inv = 1.0f / l_tot;
-  const int64_t wrow = (int64_t)it.unit * P.lmax + tq_row;
-  _Float16* orow = reinterpret_cast<_Float16*>(a.ws + P.o_off) + wrow * D;
+  char* stg = reinterpret_cast<char*>(&sm.k[0][0]) + wv * 32 * TL::kRowBytes;
+  auto stg_off = [&](int row, int chunk) {
+    return row * TL::kRowBytes + ((chunk ^ ((row >> 1) & (TL::kSlots - 1))) << 4);
+  };
 #pragma unroll
   for (int db = 0; db < DB; ++db)
 #pragma unroll
@@ -519,10 +525,21 @@ __global__ __launch_bounds__(kThreads) void attn_fwd_bf16(AttnArgs a) {
       f16x4 o;
 #pragma unroll
       for (int e = 0; e < 4; ++e) o[e] = (_Float16)(acc_o[db][4 * jj + e] * inv);
-      *reinterpret_cast<f16x4*>(orow + db * 32 + 8 * jj + 4 * hi) = o;
+      *reinterpret_cast<f16x4*>(stg + stg_off(qr, db * 4 + jj) + 8 * hi) = o;
     }
-  if (hi == 0)
-    reinterpret_cast<float*>(a.ws + P.lse_off)[wrow] = (m_run + __builtin_amdgcn_logf(l_tot)) * kLn2;
+  if (hi == 0 && q_valid)
+    reinterpret_cast<float*>(a.ws + P.lse_off)[(int64_t)it.unit * P.lmax + tq_row] =
+        (m_run + __builtin_amdgcn_logf(l_tot)) * kLn2;
+  // Each pass writes 64 consecutive 16-byte chunks: 1024 / (2 D) rows.
+  constexpr int kPasses = 32 * TL::kRowBytes / 1024;
+  _Float16* obase = reinterpret_cast<_Float16*>(a.ws + P.o_off) + ((int64_t)it.unit * P.lmax + wq_lo) * D;
+#pragma unroll
+  for (int i = 0; i < kPasses; ++i) {
+    const int row = (i * 64 + lane) / TL::kSlots;
+    const int chunk = (i * 64 + lane) % TL::kSlots;
+    const u32x4 x = *reinterpret_cast<const u32x4*>(stg + stg_off(row, chunk));
+    if (wq_lo + row < L) *reinterpret_cast<u32x4*>(obase + row * D + chunk * 8) = x;
+  }
 }
 
 // ---------------------------------------------------------------------------
