@@ -1,47 +1,30 @@
 // Stage 1 of the dilated-attention forward pass on gfx950: per pattern, per
 // (batch, head, segment), gather the kept rows (every r-th row from the head's
-// offset, Sec. 2.2 Eqs. 3-5 and Sec. 2.3) straight from HBM into registers and
-// LDS, and run softmax attention on them (Sec. 2.2 Eq. 6) with an online
-// softmax.  The normalised output rows and their log-sum-exp go to the
-// workspace in compact per-pattern order [b][h][segment][t][D].
+// offset, Sec. 2.2 Eqs. 3-5 and Sec. 2.3) straight from HBM into LDS, and run
+// softmax attention on them (Sec. 2.2 Eq. 6) with an online softmax.  The
+// normalised output rows and their log-sum-exp go to the workspace in compact
+// per-pattern order [b][h][segment][t][D].
 //
 // bf16 path: one work item = 128 query rows of one sparsified segment, four
 // waves of 32 rows.  Scores are computed transposed, S^T = K Q^T, with
 // v_mfma_f32_32x32x16_bf16, so that every lane owns one query row: the row
 // max needs one exchange between the two half-waves and the probabilities can
 // feed the P V product (computed as O^T = V^T P^T) straight from registers.
-// V is stored transposed in LDS, with keys permuted inside each group of 16
-// so a lane's eight keys of one MFMA step are contiguous.
+// K and V tiles are loaded from HBM into LDS without passing through
+// registers; V^T fragments come from transposed LDS reads.
 //
 // f32 path: a plain VALU kernel (one thread per query row) used for float32
 // inputs, where accuracy rather than speed is the point.
 #include <hip/hip_runtime.h>
 
 #include <algorithm>
-#include <type_traits>
 
-#include "kernels.h"
+#include "device_common.h"
 
 namespace da {
 namespace {
 
-typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
-typedef float f32x16 __attribute__((ext_vector_type(16)));
-typedef float f32x4 __attribute__((ext_vector_type(4)));
-typedef _Float16 f16x4 __attribute__((ext_vector_type(4)));
-typedef unsigned int u32x4 __attribute__((ext_vector_type(4)));
-typedef unsigned int u32x2 __attribute__((ext_vector_type(2)));
-typedef unsigned short u16;
-
-constexpr float kLn2 = 0.693147180559945309f;
-constexpr float kLog2e = 1.442695040888963407f;
 constexpr float kNegBig = -1.0e30f;   // finite "minus infinity" for running maxima
-
-struct PatArgs {
-  int32_t w, r, nseg, lmax, ntiles, units;
-  int64_t o_off;    // byte offset of this pattern's output rows in the workspace
-  int64_t lse_off;  // byte offset of this pattern's lse in the workspace
-};
 
 struct AttnArgs {
   const void* q;
@@ -54,109 +37,6 @@ struct AttnArgs {
   // only use a pattern's index to find its record here).
   PatArgs pat[DA_MAX_PATTERNS];
 };
-
-// One attention work item: which segment of which pattern, and which query tile.
-struct Item {
-  int pi;          // pattern index
-  int b, h, g;     // batch, head, segment
-  int unit;        // (b*H + h)*nseg + g
-  int tq;          // query tile index inside the segment
-  int L;           // kept rows of this (head, segment)
-  int64_t row0;    // [B,N,H] row index of kept row t = 0
-  int64_t rstride; // row-index step between consecutive kept rows (r*H)
-};
-
-// Workgroups are handed to the eight XCDs round-robin (launch index mod 8),
-// so launch index x is mapped to XCD c = x mod 8 and the units with index = c
-// (mod 8) are given to that XCD: the query tiles of one segment run on one
-// XCD and its K/V rows are fetched into that XCD's L2 once.  (A pattern whose
-// unit count is not a multiple of 8 has its long query tiles dealt to the
-// XCDs one by one instead, trading L2 reuse for balance.)  On each XCD the
-// items come in two phases.  First, pattern by pattern (in the order of the
-// records, those with the most query tiles per segment first) and unit by unit, the query tiles from the
-// last (the longest under a causal mask) down to tile kShortTiles, so the
-// tiles of a segment run close together in time.  Then
-// the first kShortTiles query tiles of every unit, level by level from tile
-// kShortTiles - 1 down to tile 0: the shortest items are dispatched last and
-// fill the gaps as the longer ones drain.
-constexpr int kShortTiles = 3;
-
-// Number of units of a pattern that XCD c owns.
-__device__ inline int units_on_xcd(const PatArgs& P, int c) {
-  return P.units > c ? (P.units - c + 7) >> 3 : 0;
-}
-
-__device__ inline bool decode_item(const AttnArgs& a, int bid, int block_m, Item& it) {
-  const int c = bid & 7;
-  int slot = bid >> 3;
-  int pi = -1, unit = 0, tq = 0;
-  // Fully unrolled: the records are read with constant offsets, in a few
-  // scalar loads issued together.
-#pragma unroll
-  for (int p = 0; p < DA_MAX_PATTERNS; ++p) {
-    if (p >= a.npat) break;
-    const PatArgs& P = a.pat[p];
-    const int nlong = P.ntiles > kShortTiles ? P.ntiles - kShortTiles : 0;
-    if ((P.units & 7) == 0) {
-      const int n = units_on_xcd(P, c) * nlong;
-      if (slot < n) {
-        pi = p;
-        const int j = slot / nlong;
-        unit = c + 8 * j;
-        tq = P.ntiles - 1 - (slot - j * nlong);
-        break;
-      }
-      slot -= n;
-    } else {
-      // A unit count that is not a multiple of 8 would load the XCDs
-      // unevenly: the pattern's long items f = unit * nlong + (ntiles-1-tq)
-      // are dealt to the XCDs one by one instead (f = c mod 8 to XCD c).
-      const int total = P.units * nlong;
-      const int n = total > c ? (total - c + 7) >> 3 : 0;
-      if (slot < n) {
-        pi = p;
-        const int f = c + 8 * slot;
-        unit = f / nlong;
-        tq = P.ntiles - 1 - (f - unit * nlong);
-        break;
-      }
-      slot -= n;
-    }
-  }
-#pragma unroll
-  for (int t = kShortTiles - 1; t >= 0; --t) {
-    if (pi >= 0) break;
-#pragma unroll
-    for (int p = 0; p < DA_MAX_PATTERNS; ++p) {
-      if (p >= a.npat) break;
-      const PatArgs& P = a.pat[p];
-      const int n = P.ntiles > t ? units_on_xcd(P, c) : 0;
-      if (slot < n) {
-        pi = p;
-        unit = c + 8 * slot;
-        tq = t;
-        break;
-      }
-      slot -= n;
-    }
-  }
-  if (pi < 0) return false;
-  const PatArgs& P = a.pat[pi];
-  it.tq = tq;
-  it.pi = pi;
-  it.unit = unit;
-  it.g = unit % P.nseg;
-  const int bh = unit / P.nseg;
-  it.h = bh % a.H;
-  it.b = bh / a.H;
-  const int s = it.h % P.r;
-  const int seg_start = it.g * P.w;
-  const int seg_len = min(P.w, a.N - seg_start);
-  it.L = seg_len > s ? (seg_len - s + P.r - 1) / P.r : 0;
-  it.row0 = ((int64_t)it.b * a.N + seg_start + s) * a.H + it.h;
-  it.rstride = (int64_t)P.r * a.H;
-  return it.tq * block_m < it.L;
-}
 
 // ---------------------------------------------------------------------------
 // bf16 MFMA kernel
@@ -172,92 +52,11 @@ constexpr int kBN = DA_KEY_TILE;  // keys per K/V tile
 // bf16 and the fp32 sums hold exactly as well as values below 1.
 constexpr float kRescaleSlack = 8.0f;
 
-// K and V tiles live in LDS row-major (kBN rows of D bf16), without padding:
-// a row is D/8 16-byte slots and logical slot c of row k is stored at slot
-// c ^ swz(k).  LDS serves 256 bytes per cycle from 64 four-byte banks, i.e.
-// sixteen 16-byte bank groups; a 16-byte read is served 16 lanes per cycle,
-// an 8-byte read 32 lanes per cycle.  swz(k) makes both access patterns of
-// the kernel conflict-free:
-//   K fragments: 16 consecutive rows at one logical slot -> 16 bank groups;
-//   V^T reads:   4 consecutive rows (aligned) x 4 consecutive slots -> 16.
-// Row k starts at bank group (k * D/8) mod 16, which swz(k) complements; it
-// depends on bits 0-3 of k only, so rows 16 apart share it.
-template <int D>
-struct TileLayout {
-  static constexpr int kSlots = D / 8;                     // 16-byte slots per row
-  static constexpr int kRowBytes = D * 2;
-  static constexpr int kTileBytes = kBN * kRowBytes;
-  __device__ static int swz(int row) {
-    if constexpr (D == 32) return (row >> 2) & 3;
-    else if constexpr (D == 64) return (((row >> 1) & 1) << 2) | ((row >> 2) & 3);
-    else return ((row & 3) << 2) | ((row >> 2) & 3);
-  }
-  __device__ static int offset(int row, int slot) {        // byte offset of a slot
-    return row * kRowBytes + ((slot ^ swz(row)) << 4);
-  }
-};
-
 template <int D>
 struct SmemBf16 {
   __attribute__((aligned(16))) u16 k[2][kBN * D];  // double-buffered K tiles
   __attribute__((aligned(16))) u16 v[2][kBN * D];  // double-buffered V tiles
 };
-
-typedef __attribute__((address_space(3))) void lds_void;
-
-__device__ inline u32x4 load16(const u16* p) { return *reinterpret_cast<const u32x4*>(p); }
-
-// The value held by lane l ^ 32 (the other half-wave), via v_permlane32_swap.
-__device__ inline float other_half(float x) {
-  const unsigned u = __builtin_bit_cast(unsigned, x);
-  const auto sw = __builtin_amdgcn_permlane32_swap(u, u, false, false);
-  const unsigned lane = __builtin_amdgcn_mbcnt_hi(~0u, __builtin_amdgcn_mbcnt_lo(~0u, 0u));
-  return __builtin_bit_cast(float, lane < 32 ? sw[1] : sw[0]);
-}
-
-// LDS byte address of a pointer into a __shared__ array.
-__device__ inline uint32_t lds_addr(const void* p) {
-  return static_cast<uint32_t>(reinterpret_cast<size_t>((const lds_void*)p));
-}
-
-// ds_read_b64_tr_b16 at a VGPR address plus a constant byte offset.  Within
-// each 16-lane group, lane 4r + c supplies the address of four consecutive
-// 16-bit elements of row r (c = 0..3) and receives element c of each of the
-// four rows.  Issued as inline assembly: the compiler's builtin for this
-// instruction makes it wait for every outstanding HBM-to-LDS load first,
-// including the prefetch of the next tile, which it cannot tell apart from
-// the tile being read.  The results are therefore not tracked by the
-// compiler; lds_wait<N>() followed by lds_bind() on each result makes them
-// usable once at most N LDS operations of this wave are still outstanding
-// (LDS operations complete in order).
-template <int kOff>
-__device__ inline u32x2 lds_read_tr16(uint32_t addr) {
-  u32x2 r;
-  asm volatile("ds_read_b64_tr_b16 %0, %1 offset:%2" : "=v"(r) : "v"(addr), "i"(kOff) : "memory");
-  return r;
-}
-template <int N>
-__device__ inline void lds_wait() {
-  asm volatile("s_waitcnt lgkmcnt(%0)" ::"i"(N) : "memory");
-}
-__device__ inline void lds_bind(u32x2& r) { asm volatile("" : "+v"(r)); }
-
-// Calls f(std::integral_constant<int, I>) for I = 0 .. N-1, so that the index
-// can form a constant operand.
-template <int I, int N, typename F>
-__device__ inline void static_for(F&& f) {
-  if constexpr (I < N) {
-    f(std::integral_constant<int, I>{});
-    static_for<I + 1, N>(f);
-  }
-}
-
-// Word 3 of a raw buffer resource on gfx9-family GPUs (32-bit data format,
-// no swizzle); with stride 0 the size field is a byte count and reads at or
-// beyond it return zero.
-constexpr int kBufferFlags = 0x00020000;
-// s_waitcnt immediate: vmcnt(0), expcnt and lgkmcnt left at their maxima.
-constexpr int kWaitVmcnt0 = 0x0F70;
 
 template <int D, bool kBufferLoads>
 __global__ __launch_bounds__(kThreads) void attn_fwd_bf16(AttnArgs a) {
