@@ -1,4 +1,4 @@
-"""CPU oracle for LongNet dilated attention (forward).  TEST INFRASTRUCTURE ONLY.
+"""CPU oracle for LongNet dilated attention (forward and backward).  TEST INFRASTRUCTURE ONLY.
 
 Only the tests, the smoke check and the benchmark's CPU-baseline leg may import
 this package.  The product path (the HIP library and its Python binding) never
@@ -21,3 +21,10 @@ from .dilated_ref import (  # noqa: F401
 )
 from .brute import brute_mask_ref, brute_multiset_ref, visible_multiset  # noqa: F401
 from .accounting import exact_causal_pairs, sparse_flops, covered_rows  # noqa: F401
+from .dilated_bwd import (  # noqa: F401
+    delta_ref,
+    attend_bwd,
+    dilated_attention_bwd_ref,
+    dq_rows_ref,
+    dkdv_rows_ref,
+)
