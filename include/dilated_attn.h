@@ -1,5 +1,6 @@
 /*
- * dilated_attn.h - C ABI of the MI355X (gfx950) dilated-attention forward pass.
+ * dilated_attn.h - C ABI of the MI355X (gfx950) dilated-attention forward and
+ * backward passes.
  *
  * The operator is LongNet's dilated attention (Sec. 2.2-2.3 of the paper):
  *   1. split the sequence into segments of length w_i          (Sec. 2.2, Eqs. 3-5)
@@ -110,6 +111,66 @@ int dilated_attn_plan(int64_t B, int64_t N, int64_t H, int64_t D,
  */
 int dilated_attn_fwd(const void* q, const void* k, const void* v, void* out,
                      float* lse, int64_t B, int64_t N, int64_t H, int64_t D,
+                     const da_pattern_t* patterns, int64_t num_patterns,
+                     int64_t causal, int64_t dtype, float softmax_scale,
+                     void* workspace, uint64_t workspace_bytes, void* stream);
+
+/*
+ * Backward pass: gradients of a loss with respect to q, k and v, given the
+ * gradient dout of the loss with respect to out.
+ *
+ * The mixture of Eqs. 9-10 is one softmax over the multiset of (pattern, key)
+ * pairs a query sees (Sec. 2.2, after Eq. 10), so with the combined lse of
+ * the forward pass and delta = sum_d dout * out per row, each pattern's
+ * contribution is the softmax-attention derivative on its sparsified
+ * segments: P = exp(scale q.k - lse), dS = P (dout.v - delta),
+ * dq += scale dS k, dk += scale dS q, dv += P dout; a row collects the
+ * contributions of every pattern that keeps it (the paper's distributed
+ * algorithm has this backward, Sec. 3.1).
+ *
+ * This build computes the backward for dtype DA_BF16 and D in {32, 64}; other
+ * head dims and DA_F32 return DA_EUNSUPPORTED.
+ */
+
+/*
+ * dilated_attn_bwd_plan - validate a backward problem and report its
+ * workspace and work.  Host only; arguments as for dilated_attn_plan.  Fills
+ * *info: workspace_bytes for dilated_attn_bwd, num_work_items = the dq and
+ * the dk/dv kernels' work items, covered_rows, sparse_flops = 10*D per
+ * unmasked (query, key) pair (the five products of the derivative),
+ * bytes_attn = algorithmic HBM bytes of the two gradient kernels and
+ * bytes_combine = those of the delta and gradient-sum kernels.
+ */
+int dilated_attn_bwd_plan(int64_t B, int64_t N, int64_t H, int64_t D,
+                          const da_pattern_t* patterns, int64_t num_patterns,
+                          int64_t causal, int64_t dtype, float softmax_scale,
+                          da_plan_info_t* info);
+
+/*
+ * dilated_attn_bwd - dilated-attention backward pass.
+ *
+ * q, k, v     device pointers, [B, N, H, D] of dtype, read only: the
+ *             forward's inputs.
+ * out, lse    device pointers, the forward's outputs for these inputs
+ *             ([B, N, H, D] of dtype and [B, H, N] float32), read only.
+ * dout        device pointer, [B, N, H, D] of dtype, read only.
+ * dq, dk, dv  device pointers, [B, N, H, D] of dtype, written (every
+ *             element; rows no pattern keeps get 0).
+ * patterns, causal, dtype, softmax_scale: those of the forward call.
+ * workspace   device scratch of at least info.workspace_bytes from
+ *             dilated_attn_bwd_plan, owned by the caller; contents on entry
+ *             are ignored and on return are unspecified.
+ * stream      a hipStream_t (NULL = the default stream), asynchronous as for
+ *             dilated_attn_fwd.
+ *
+ * All device pointers must be 16-byte aligned; dq, dk and dv must not overlap
+ * each other or any input.  Returns DA_OK or a negative error code; every
+ * argument is checked before any launch and an error leaves all buffers
+ * untouched.
+ */
+int dilated_attn_bwd(const void* q, const void* k, const void* v, const void* out,
+                     const float* lse, const void* dout, void* dq, void* dk, void* dv,
+                     int64_t B, int64_t N, int64_t H, int64_t D,
                      const da_pattern_t* patterns, int64_t num_patterns,
                      int64_t causal, int64_t dtype, float softmax_scale,
                      void* workspace, uint64_t workspace_bytes, void* stream);

@@ -32,7 +32,7 @@ from typing import Iterable, List, Sequence, Tuple
 
 import numpy as np
 
-from .dilated_ref import (Pattern, default_scale, dilated_attention_ref, dilated_attention_rows_ref,
+from .dilated_ref import (Pattern, _rows, default_scale, dilated_attention_ref, dilated_attention_rows_ref,
                           head_offset, index_set, num_segments, segment_bounds)
 
 
@@ -91,7 +91,8 @@ def dilated_attention_bwd_ref(q, k, v, dout, patterns: Sequence[Pattern], causal
 
 
 def _rows_of(x, b, idx, h):
-    return np.asarray(x[b, idx, h, :], dtype=np.float64)
+    """Rows x[b, idx, h, :] as float64 NumPy (x a NumPy array or a CPU tensor)."""
+    return _rows(x, b, np.asarray(idx, dtype=np.int64), h)
 
 
 def _kept_position(p: int, w: int, r: int, h: int):

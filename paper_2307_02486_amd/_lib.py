@@ -62,6 +62,11 @@ def load():
     lib.dilated_attn_fwd.argtypes = [vp, vp, vp, vp, vp, i64, i64, i64, i64, ctypes.POINTER(Pattern),
                                      i64, i64, i64, f32, vp, ctypes.c_uint64, vp]
     lib.dilated_attn_fwd.restype = ctypes.c_int
+    lib.dilated_attn_bwd_plan.argtypes = lib.dilated_attn_plan.argtypes
+    lib.dilated_attn_bwd_plan.restype = ctypes.c_int
+    lib.dilated_attn_bwd.argtypes = [vp, vp, vp, vp, vp, vp, vp, vp, vp, i64, i64, i64, i64,
+                                     ctypes.POINTER(Pattern), i64, i64, i64, f32, vp, ctypes.c_uint64, vp]
+    lib.dilated_attn_bwd.restype = ctypes.c_int
     lib.dilated_attn_strerror.argtypes = [ctypes.c_int]
     lib.dilated_attn_strerror.restype = ctypes.c_char_p
     lib.dilated_attn_profile_begin.argtypes = [i64]

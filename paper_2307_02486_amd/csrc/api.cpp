@@ -1,4 +1,4 @@
-// C ABI of the dilated-attention forward pass (declared in include/dilated_attn.h).
+// C ABI of the dilated-attention forward and backward passes (declared in include/dilated_attn.h).
 #include <hip/hip_runtime.h>
 
 #include <cstdint>
@@ -87,6 +87,69 @@ int dilated_attn_fwd(const void* q, const void* k, const void* v, void* out, flo
   if (ev && hipEventRecord(ev[1], s) != hipSuccess) return DA_EHIP;
   if (da::launch_combine(p, workspace, out, lse, s) != hipSuccess) return DA_EHIP;
   if (ev && hipEventRecord(ev[2], s) != hipSuccess) return DA_EHIP;
+  return DA_OK;
+}
+
+int dilated_attn_bwd_plan(int64_t B, int64_t N, int64_t H, int64_t D, const da_pattern_t* patterns,
+                          int64_t num_patterns, int64_t causal, int64_t dtype, float softmax_scale,
+                          da_plan_info_t* info) {
+  if (!info) return DA_EINVAL;
+  da::Plan p;
+  int rc = da::make_plan(B, N, H, D, patterns, num_patterns, causal, dtype, softmax_scale, &p);
+  if (rc != DA_OK) return rc;
+  da::BwdLayout l;
+  rc = da::make_bwd_layout(p, &l);
+  if (rc != DA_OK) return rc;
+  info->workspace_bytes = l.workspace_bytes;
+  info->num_work_items = 2 * p.total_items;
+  info->covered_rows = p.covered_rows;
+  info->sparse_flops = l.flops;
+  info->bytes_attn = l.bytes_grad;
+  info->bytes_combine = l.bytes_combine;
+  return DA_OK;
+}
+
+int dilated_attn_bwd(const void* q, const void* k, const void* v, const void* out, const float* lse,
+                     const void* dout, void* dq, void* dk, void* dv, int64_t B, int64_t N, int64_t H,
+                     int64_t D, const da_pattern_t* patterns, int64_t num_patterns, int64_t causal,
+                     int64_t dtype, float softmax_scale, void* workspace, uint64_t workspace_bytes,
+                     void* stream) {
+  da::Plan p;
+  int rc = da::make_plan(B, N, H, D, patterns, num_patterns, causal, dtype, softmax_scale, &p);
+  if (rc != DA_OK) return rc;
+  da::BwdLayout l;
+  rc = da::make_bwd_layout(p, &l);
+  if (rc != DA_OK) return rc;
+  const void* ins[6] = {q, k, v, out, lse, dout};
+  void* outs[3] = {dq, dk, dv};
+  for (const void* x : ins)
+    if (!x) return DA_EINVAL;
+  for (const void* x : outs)
+    if (!x) return DA_EINVAL;
+  if (!workspace) return DA_EINVAL;
+  for (const void* x : ins)
+    if (!aligned16(x)) return DA_EALIGN;
+  for (const void* x : outs)
+    if (!aligned16(x)) return DA_EALIGN;
+  if (!aligned16(workspace)) return DA_EALIGN;
+  const uint64_t tb = static_cast<uint64_t>(B * N * H * D) * 2;
+  const uint64_t lb = static_cast<uint64_t>(B * H * N) * 4;
+  const uint64_t in_sizes[6] = {tb, tb, tb, tb, lb, tb};
+  for (int i = 0; i < 3; ++i) {
+    for (int j = 0; j < 6; ++j)
+      if (overlaps(outs[i], tb, ins[j], in_sizes[j])) return DA_EINVAL;
+    for (int j = i + 1; j < 3; ++j)
+      if (overlaps(outs[i], tb, outs[j], tb)) return DA_EINVAL;
+  }
+  if (workspace_bytes < l.workspace_bytes) return DA_EWORKSPACE;
+  for (int j = 0; j < 6; ++j)
+    if (overlaps(workspace, l.workspace_bytes, ins[j], in_sizes[j])) return DA_EINVAL;
+  for (int i = 0; i < 3; ++i)
+    if (overlaps(workspace, l.workspace_bytes, outs[i], tb)) return DA_EINVAL;
+
+  hipStream_t s = static_cast<hipStream_t>(stream);
+  if (da::launch_backward(p, l, q, k, v, out, lse, dout, dq, dk, dv, workspace, s) != hipSuccess)
+    return DA_EHIP;
   return DA_OK;
 }
 

@@ -38,6 +38,7 @@ struct Item {
   int L;           // kept rows of this (head, segment)
   int64_t row0;    // [B,N,H] row index of kept row t = 0
   int64_t rstride; // row-index step between consecutive kept rows (r*H)
+  int p0;          // sequence position of kept row t = 0
 };
 
 // Workgroups are handed to the eight XCDs round-robin (launch index mod 8),
@@ -56,7 +57,8 @@ struct Item {
 constexpr int kShortTiles = 3;
 
 // Number of units of a pattern that XCD c owns.
-__device__ inline int units_on_xcd(const PatArgs& P, int c) {
+template <typename Pat>
+__device__ inline int units_on_xcd(const Pat& P, int c) {
   return P.units > c ? (P.units - c + 7) >> 3 : 0;
 }
 
@@ -70,7 +72,7 @@ __device__ inline bool decode_item(const Args& a, int bid, int block_m, Item& it
 #pragma unroll
   for (int p = 0; p < DA_MAX_PATTERNS; ++p) {
     if (p >= a.npat) break;
-    const PatArgs& P = a.pat[p];
+    const auto& P = a.pat[p];
     const int nlong = P.ntiles > kShortTiles ? P.ntiles - kShortTiles : 0;
     if ((P.units & 7) == 0) {
       const int n = units_on_xcd(P, c) * nlong;
@@ -104,7 +106,7 @@ __device__ inline bool decode_item(const Args& a, int bid, int block_m, Item& it
 #pragma unroll
     for (int p = 0; p < DA_MAX_PATTERNS; ++p) {
       if (p >= a.npat) break;
-      const PatArgs& P = a.pat[p];
+      const auto& P = a.pat[p];
       const int n = P.ntiles > t ? units_on_xcd(P, c) : 0;
       if (slot < n) {
         pi = p;
@@ -116,7 +118,7 @@ __device__ inline bool decode_item(const Args& a, int bid, int block_m, Item& it
     }
   }
   if (pi < 0) return false;
-  const PatArgs& P = a.pat[pi];
+  const auto& P = a.pat[pi];
   it.tq = tq;
   it.pi = pi;
   it.unit = unit;
@@ -130,6 +132,7 @@ __device__ inline bool decode_item(const Args& a, int bid, int block_m, Item& it
   it.L = seg_len > s ? (seg_len - s + P.r - 1) / P.r : 0;
   it.row0 = ((int64_t)it.b * a.N + seg_start + s) * a.H + it.h;
   it.rstride = (int64_t)P.r * a.H;
+  it.p0 = seg_start + s;
   return it.tq * block_m < it.L;
 }
 

@@ -1,4 +1,4 @@
-// Launchers of the two device stages of the dilated-attention forward pass.
+// Launchers of the device stages of the dilated-attention forward and backward passes.
 #pragma once
 
 #include <hip/hip_runtime.h>
@@ -18,5 +18,11 @@ hipError_t launch_attention(const Plan& plan, const void* q, const void* k, cons
 // (Sec. 2.2, Eqs. 7-10).
 hipError_t launch_combine(const Plan& plan, const void* workspace, void* out, float* lse,
                           hipStream_t stream);
+
+// Backward: per-row -delta and -lse*log2(e), the per-pattern dq and dk/dv
+// kernels into compact workspace rows, and their sum per row into dq, dk, dv.
+hipError_t launch_backward(const Plan& plan, const BwdLayout& lay, const void* q, const void* k,
+                           const void* v, const void* out, const float* lse, const void* dout, void* dq,
+                           void* dk, void* dv, void* workspace, hipStream_t stream);
 
 }  // namespace da

@@ -126,4 +126,44 @@ int make_plan(int64_t B, int64_t N, int64_t H, int64_t D, const da_pattern_t* pa
   return DA_OK;
 }
 
+int make_bwd_layout(const Plan& p, BwdLayout* out) {
+  if (!out) return DA_EINVAL;
+  if (p.dtype != DA_BF16 || (p.D != 32 && p.D != 64)) return DA_EUNSUPPORTED;
+  // 32-bit offsets inside a tile of 64 kept rows (rows r*H*D elements apart,
+  // and the rows' per-row scalars r floats apart)
+  if (!p.offsets32) return DA_EUNSUPPORTED;
+  for (int i = 0; i < p.npat; ++i)
+    if (static_cast<double>(p.pat[i].r) * 4.0 * 65.0 >= 2147483648.0) return DA_EUNSUPPORTED;
+  BwdLayout l;
+  std::memset(&l, 0, sizeof(l));
+  const uint64_t rows_all = static_cast<uint64_t>(p.B) * p.N * p.H;
+  uint64_t ws = 0;
+  l.nl2_off = ws;
+  ws = align_up(ws + rows_all * 4);
+  l.nd_off = ws;
+  ws = align_up(ws + rows_all * 4);
+  for (int i = 0; i < p.npat; ++i) {
+    const uint64_t rows = static_cast<uint64_t>(p.pat[i].units) * static_cast<uint64_t>(p.pat[i].lmax);
+    const uint64_t bytes = rows * static_cast<uint64_t>(p.D) * 4;
+    l.dq_off[i] = ws;
+    ws = align_up(ws + bytes);
+    l.dk_off[i] = ws;
+    ws = align_up(ws + bytes);
+    l.dv_off[i] = ws;
+    ws = align_up(ws + bytes);
+  }
+  l.workspace_bytes = ws;
+  const double D = static_cast<double>(p.D), es = 2.0, cov = static_cast<double>(p.covered_rows);
+  l.flops = 2.5 * p.sparse_flops;
+  // each gradient kernel reads the kept q, k, v, dout rows once and the two
+  // per-row scalars; dq writes one float32 row, dk/dv two
+  l.bytes_grad = cov * (2.0 * (4.0 * D * es + 8.0) + 3.0 * D * 4.0);
+  // delta: out, dout and lse of every row read, two scalars written; sum:
+  // the compact gradients read, dq, dk, dv written
+  l.bytes_combine = static_cast<double>(rows_all) * (2.0 * D * es + 4.0 + 8.0 + 3.0 * D * es) +
+                    cov * 3.0 * D * 4.0;
+  *out = l;
+  return DA_OK;
+}
+
 }  // namespace da

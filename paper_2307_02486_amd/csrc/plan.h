@@ -64,6 +64,25 @@ struct Plan {
   double bytes_combine;
 };
 
+// Workspace of a backward call: per (b, h, row) -lse*log2(e) and -delta
+// (float32, [B][H][N] each), then per pattern the compact float32 gradients
+// of its kept rows, [units][lmax][D] for dq, dk and dv.
+struct BwdLayout {
+  uint64_t nl2_off;   // byte offset of -lse*log2(e)
+  uint64_t nd_off;    // byte offset of -delta
+  uint64_t dq_off[DA_MAX_PATTERNS];
+  uint64_t dk_off[DA_MAX_PATTERNS];
+  uint64_t dv_off[DA_MAX_PATTERNS];
+  uint64_t workspace_bytes;
+  double flops;          // 10*D per unmasked pair
+  double bytes_grad;     // algorithmic HBM bytes of the dq and dk/dv kernels
+  double bytes_combine;  // algorithmic HBM bytes of the delta and sum kernels
+};
+
+// Backward workspace and work of a validated forward plan.  DA_EUNSUPPORTED
+// unless the plan is bf16 with D in {32, 64}.
+int make_bwd_layout(const Plan& p, BwdLayout* out);
+
 // Query rows per work item of the attention kernel for a dtype.
 int block_m_for(int dtype);
 

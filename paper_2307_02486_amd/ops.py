@@ -1,7 +1,8 @@
-"""Python entry points of the dilated-attention forward pass.
+"""Python entry points of the dilated-attention forward and backward passes.
 
-`plan` and `dilated_attn` mirror the C ABI (dilated_attn_plan /
-dilated_attn_fwd): torch supplies device memory and the stream, every step of
+`plan`/`dilated_attn` and `plan_bwd`/`dilated_attn_bwd` mirror the C ABI
+(dilated_attn_plan / dilated_attn_fwd, dilated_attn_bwd_plan /
+dilated_attn_bwd): torch supplies device memory and the stream, every step of
 the computation runs in the HIP kernels of libdilated_attn.so.
 """
 from __future__ import annotations
@@ -112,3 +113,59 @@ class StageTimer:
             raise _lib.DilatedAttnError(rc, lib)
         self.ms_attention, self.ms_combine, self.calls = a.value, c.value, n.value
         return False
+
+
+def plan_bwd(B: int, N: int, H: int, D: int, patterns: Sequence[Tuple[int, int]], causal: bool = True,
+             dtype=torch.bfloat16, scale: float | None = None) -> dict:
+    """Validate a backward problem and return its workspace size and work (host only)."""
+    lib = _lib.load()
+    arr, n = _lib.pattern_array(patterns)
+    info = _lib.PlanInfo()
+    rc = lib.dilated_attn_bwd_plan(B, N, H, D, arr, n, int(bool(causal)), _dtype_code(dtype),
+                                   float(scale or 0.0), ctypes.byref(info))
+    if rc != 0:
+        raise _lib.DilatedAttnError(rc, lib)
+    return {k: getattr(info, k) for k, _ in _lib.PlanInfo._fields_}
+
+
+def bwd_workspace_for(q: torch.Tensor, patterns, causal=True, scale=None) -> torch.Tensor:
+    """Allocate (with torch) the device workspace a backward call on q's shape needs."""
+    B, N, H, D = q.shape
+    info = plan_bwd(B, N, H, D, patterns, causal, q.dtype, scale)
+    return torch.empty(max(256, int(info["workspace_bytes"])), dtype=torch.uint8, device=q.device)
+
+
+def dilated_attn_bwd(q: torch.Tensor, k: torch.Tensor, v: torch.Tensor, out: torch.Tensor,
+                     lse: torch.Tensor, dout: torch.Tensor, patterns: Sequence[Tuple[int, int]],
+                     causal: bool = True, scale: float | None = None, dq: torch.Tensor | None = None,
+                     dk: torch.Tensor | None = None, dv: torch.Tensor | None = None,
+                     workspace: torch.Tensor | None = None, stream: torch.cuda.Stream | None = None):
+    """Dilated-attention backward: (dq, dk, dv) given the forward's inputs and
+    outputs (out, lse) and dout, all on the GPU, [B, N, H, D] contiguous
+    (lse [B, H, N] float32).  Enqueued on `stream` and not waited for."""
+    lib = _lib.load()
+    if q.device.type != "cuda":
+        raise RuntimeError("dilated_attn_bwd runs on the GPU only; q must be a device tensor")
+    for t in (q, k, v, out, dout):
+        if not t.is_contiguous() or t.shape != q.shape or t.dtype != q.dtype or t.device != q.device:
+            raise ValueError("q, k, v, out, dout must be contiguous tensors of the same shape, dtype, device")
+    if q.dim() != 4:
+        raise ValueError("tensors must be [B, N, H, D]")
+    B, N, H, D = q.shape
+    if lse.shape != (B, H, N) or lse.dtype != torch.float32 or not lse.is_contiguous():
+        raise ValueError("lse must be a contiguous float32 [B, H, N] tensor")
+    dq = torch.empty_like(q) if dq is None else dq
+    dk = torch.empty_like(q) if dk is None else dk
+    dv = torch.empty_like(q) if dv is None else dv
+    if workspace is None:
+        workspace = bwd_workspace_for(q, patterns, causal, scale)
+    if stream is None:
+        stream = torch.cuda.current_stream(q.device)
+    arr, n = _lib.pattern_array(patterns)
+    rc = lib.dilated_attn_bwd(q.data_ptr(), k.data_ptr(), v.data_ptr(), out.data_ptr(), lse.data_ptr(),
+                              dout.data_ptr(), dq.data_ptr(), dk.data_ptr(), dv.data_ptr(), B, N, H, D,
+                              arr, n, int(bool(causal)), _dtype_code(q.dtype), float(scale or 0.0),
+                              workspace.data_ptr(), workspace.numel(), stream.cuda_stream)
+    if rc != 0:
+        raise _lib.DilatedAttnError(rc, lib)
+    return dq, dk, dv

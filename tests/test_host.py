@@ -50,7 +50,8 @@ def test_exports_every_declared_symbol(lib):
     text = open(HEADER).read()
     names = re.findall(r"^\s*(?:const\s+)?\w+\*?\s+\*?(dilated_attn_\w+)\s*\(", text, re.M)
     assert set(names) == {"dilated_attn_plan", "dilated_attn_fwd", "dilated_attn_strerror",
-                          "dilated_attn_profile_begin", "dilated_attn_profile_end"}
+                          "dilated_attn_profile_begin", "dilated_attn_profile_end",
+                          "dilated_attn_bwd_plan", "dilated_attn_bwd"}
     for n in names:
         assert hasattr(lib, n), n
     nm = subprocess.run(["nm", "-D", "--defined-only", os.path.join(ROOT, "paper_2307_02486_amd",
@@ -155,3 +156,52 @@ def test_profile_window_arguments(lib):
     assert lib.dilated_attn_profile_begin(0) == -1
     assert lib.dilated_attn_profile_begin(1 << 21) == -1
     assert lib.dilated_attn_profile_end(None, None, None) == -1   # no window open
+
+
+def test_bwd_plan_accounting():
+    """Backward workspace = two [B,H,N] float32 arrays plus, per pattern, three
+    float32 [units][lmax][D] blocks, each 256-byte aligned; flops = 10 D per pair."""
+    from paper_2307_02486_amd import plan, plan_bwd
+    import torch
+    for (B, N, H, D, pats) in [(1, 32768, 12, 64, [(2048, 1), (4096, 2), (8192, 4), (16384, 6), (32768, 12)]),
+                               (2, 777, 5, 32, [(256, 1), (512, 7), (1000, 9)])]:
+        f = plan(B, N, H, D, pats, True, torch.bfloat16)
+        b = plan_bwd(B, N, H, D, pats, True, torch.bfloat16)
+        al = lambda x: (x + 255) // 256 * 256
+        ws = al(al(B * H * N * 4) + B * H * N * 4)
+        for (w, r) in pats:
+            w = min(w, N)
+            rows = B * H * (-(-N // w)) * (-(-w // r))
+            for _ in range(3):
+                ws = al(ws + rows * D * 4)
+        assert b["workspace_bytes"] == ws
+        assert b["sparse_flops"] == pytest.approx(2.5 * f["sparse_flops"], rel=1e-12)
+        assert b["covered_rows"] == f["covered_rows"]
+        assert b["num_work_items"] == 2 * f["num_work_items"]
+
+
+def test_bwd_unsupported_and_errors(lib):
+    """The backward covers bf16 with D in {32, 64}; argument errors return
+    before any HIP call (fake, never dereferenced pointers)."""
+    from paper_2307_02486_amd import _lib, plan_raw
+    arr, n = _lib.pattern_array([(8, 1)])
+    info = _lib.PlanInfo()
+    import ctypes
+    assert _lib.ERRORS[lib.dilated_attn_bwd_plan(1, 16, 2, 128, arr, n, 1, 1, 0.0, ctypes.byref(info))] == \
+        "DA_EUNSUPPORTED"
+    assert _lib.ERRORS[lib.dilated_attn_bwd_plan(1, 16, 2, 64, arr, n, 1, 0, 0.0, ctypes.byref(info))] == \
+        "DA_EUNSUPPORTED"
+    assert lib.dilated_attn_bwd_plan(1, 16, 2, 64, arr, n, 1, 1, 0.0, ctypes.byref(info)) == 0
+    good = [0x10000 * (i + 1) for i in range(9)]   # q k v out lse dout dq dk dv
+    def call(ptrs, ws=0x1000000, ws_bytes=1 << 20, D=64, dtype=1):
+        return lib.dilated_attn_bwd(*ptrs, 1, 16, 2, D, arr, n, 1, dtype, 0.0, ws, ws_bytes, None)
+    assert _lib.ERRORS[call([0] + good[1:])] == "DA_EINVAL"
+    assert _lib.ERRORS[call(good[:8] + [0])] == "DA_EINVAL"
+    assert _lib.ERRORS[call(good, ws=0)] == "DA_EINVAL"
+    assert _lib.ERRORS[call(good[:6] + [good[6] + 4] + good[7:])] == "DA_EALIGN"
+    assert _lib.ERRORS[call(good, ws_bytes=16)] == "DA_EWORKSPACE"
+    assert _lib.ERRORS[call(good[:6] + [good[0]] + good[7:])] == "DA_EINVAL"     # dq aliases q
+    assert _lib.ERRORS[call(good[:7] + [good[6]] + good[8:])] == "DA_EINVAL"     # dk aliases dq
+    assert _lib.ERRORS[call(good, ws=good[5])] == "DA_EINVAL"                     # workspace aliases dout
+    assert _lib.ERRORS[call(good, D=128)] == "DA_EUNSUPPORTED"
+    assert _lib.ERRORS[call(good, dtype=0)] == "DA_EUNSUPPORTED"
