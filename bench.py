@@ -45,6 +45,8 @@ def parse():
     ap.add_argument("--sweep", action="store_true",
                     help="instead of the benchmark: the dense-versus-dilated sweep over N = 8K..1M "
                          "(fixed tokens per batch), one JSON line per (N, variant)")
+    ap.add_argument("--backward", action="store_true",
+                    help="instead of the benchmark: time the backward pass on the workload, one JSON line")
     ap.add_argument("--copy-calibration-mib", type=int, default=0,
                     help="only run a plain device-to-device copy of this many MiB (5 times), to "
                          "calibrate the HBM byte counters of a profiler against a known size")
@@ -201,6 +203,60 @@ def sweep(args):
             torch.cuda.empty_cache()
 
 
+def backward(args):
+    """Backward pass on the workload: `warmup` untimed calls, then `steps`
+    back-to-back calls timed with events on the stream; effective TFLOP/s over
+    10*D per unmasked pair (the five products of the derivative)."""
+    import statistics
+
+    import torch
+
+    import workloads
+    from paper_2307_02486_amd import bwd_workspace_for, dilated_attn, dilated_attn_bwd, plan_bwd
+    wl = workloads.BY_NAME[args.workload]
+    dev = torch.device("cuda:0")
+    torch.cuda.set_device(dev)
+    stream = torch.cuda.current_stream(dev)
+    q, k, v = workloads.make_qkv(wl, device=dev)
+    dout = workloads.make_random(q.shape, wl.torch_dtype, 1.0, wl.seed, dev, 3)
+    pats = list(wl.patterns)
+    out, lse = dilated_attn(q, k, v, pats, wl.causal, stream=stream)
+    info = plan_bwd(wl.B, wl.N, wl.H, wl.D, pats, wl.causal, wl.torch_dtype)
+    ws = bwd_workspace_for(q, pats, wl.causal)
+    dq, dk, dv = torch.empty_like(q), torch.empty_like(q), torch.empty_like(q)
+
+    def step():
+        dilated_attn_bwd(q, k, v, out, lse, dout, pats, wl.causal, dq=dq, dk=dk, dv=dv, workspace=ws, stream=stream)
+
+    for _ in range(args.warmup):
+        step()
+    torch.cuda.synchronize()
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    e0.record(stream)
+    for _ in range(args.steps):
+        step()
+    e1.record(stream)
+    torch.cuda.synchronize()
+    ms = e0.elapsed_time(e1) / args.steps
+    single = []
+    for _ in range(min(args.steps, 20)):
+        a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        a.record(stream)
+        step()
+        b.record(stream)
+        b.synchronize()
+        single.append(a.elapsed_time(b))
+    flops = info["sparse_flops"]
+    print(json.dumps({"metric": "dilated-attn bwd effective TFLOP/s (10*D per unmasked pair)",
+                      "value": round(flops / (ms * 1e-3) / 1e12, 3), "unit": "TFLOP/s", "ms_per_step": round(ms, 5),
+                      "steps": args.steps, "warmup": args.warmup, "dtype": wl.dtype, "config": wl.describe(),
+                      "flops": flops, "tokens_per_s": round(wl.B * wl.N / (ms * 1e-3), 1),
+                      "isolated_step_ms": {"median": round(statistics.median(single), 5),
+                                           "min": round(min(single), 5)},
+                      "algorithmic_bytes": {"gradient_kernels": info["bytes_attn"],
+                                            "delta_and_sum_kernels": info["bytes_combine"]}}), flush=True)
+
+
 def main():
     args = parse()
     if args.gpus != 1:
@@ -212,6 +268,9 @@ def main():
         return
     if args.sweep:
         sweep(args)
+        return
+    if args.backward:
+        backward(args)
         return
     import torch
 
