@@ -128,8 +128,10 @@ int dilated_attn_fwd(const void* q, const void* k, const void* v, void* out,
  * contributions of every pattern that keeps it (the paper's distributed
  * algorithm has this backward, Sec. 3.1).
  *
- * This build computes the backward for dtype DA_BF16 and D in {32, 64}; other
- * head dims and DA_F32 return DA_EUNSUPPORTED.
+ * This build computes the backward for dtype DA_BF16 (D in {32, 64, 128});
+ * DA_F32 returns DA_EUNSUPPORTED, and so do patterns whose dilation makes a
+ * tile of 65 kept rows span 2 GiB or more (r*H*D*2*129 >= 2^31, or
+ * r*4*65 >= 2^31).
  */
 
 /*

@@ -1,4 +1,4 @@
-// Backward of the dilated-attention forward pass on gfx950 (bf16, D = 32/64).
+// Backward of the dilated-attention forward pass on gfx950 (bf16, D = 32/64/128).
 //
 // The mixture of the patterns (Sec. 2.2, Eqs. 9-10) is one softmax over the
 // multiset of (pattern, key) pairs a query sees (Sec. 2.2, after Eq. 10).  With
@@ -54,6 +54,24 @@ struct BwdArgs {
 };
 
 constexpr int kThreadsB = 256;  // four waves
+// Head-dim columns of dq (or dk, dv) one work item accumulates: all of them up
+// to D = 64; at D = 128 each item is run twice, once per 64-column half (the
+// scores and dP are recomputed, the accumulators fit in registers).
+template <int D>
+constexpr int kCols = D <= 64 ? D : 64;
+// Launch index of a split work item: the two halves of an item take two
+// consecutive slots of the same XCD.  Returns the item's launch index and sets
+// `half`.
+template <int D>
+__device__ inline int split_index(int bid, int& half) {
+  if constexpr (kCols<D> == D) {
+    half = 0;
+    return bid;
+  } else {
+    half = (bid >> 3) & 1;
+    return ((bid >> 4) << 3) | (bid & 7);
+  }
+}
 constexpr int kTileB = 128;     // rows (queries for dq, keys for dk/dv) per work item
 constexpr int kStepB = 64;      // rows per LDS tile of the other operand
 
@@ -162,12 +180,15 @@ __global__ __launch_bounds__(kThreadsB) void bwd_delta(DeltaArgs a) {
 template <int D>
 __global__ __launch_bounds__(kThreadsB) void bwd_dq(BwdArgs a) {
   constexpr int BN = kStepB;
-  constexpr int KC = D / 16, DB = D / 32, SB = BN / 32;
+  constexpr int KC = D / 16, DB = kCols<D> / 32, SB = BN / 32;
   using TL = TileLayout<D>;
   __shared__ SmemTiles<D> sm;
 
   Item it;
-  if (!decode_item(a, __builtin_amdgcn_workgroup_id_x(), kTileB, it)) return;
+  int half;
+  const int bid = split_index<D>(__builtin_amdgcn_workgroup_id_x(), half);
+  const int c0 = half * kCols<D>;  // first head-dim column this item accumulates
+  if (!decode_item(a, bid, kTileB, it)) return;
   const BwdPat& P = a.pat[it.pi];
   const int tid = __builtin_amdgcn_workitem_id_x();
   const int lane = tid & 63;
@@ -221,7 +242,7 @@ __global__ __launch_bounds__(kThreadsB) void bwd_dq(BwdArgs a) {
   for (int db = 0; db < DB; ++db)
 #pragma unroll
     for (int t = 0; t < 2; ++t) {
-      const int d = db * 32 + tr_d;
+      const int d = c0 + db * 32 + tr_d;
       vtr_off[db][t] = TL::offset(8 * t + 4 * hi + tr_r, d >> 3) + (d & 7) * 2;
     }
 
@@ -296,7 +317,7 @@ __global__ __launch_bounds__(kThreadsB) void bwd_dq(BwdArgs a) {
   for (int db = 0; db < DB; ++db)
 #pragma unroll
     for (int jj = 0; jj < 4; ++jj)
-      *reinterpret_cast<f32x4*>(orow + db * 32 + 8 * jj + 4 * hi) =
+      *reinterpret_cast<f32x4*>(orow + c0 + db * 32 + 8 * jj + 4 * hi) =
           f32x4{acc_dq[db][4 * jj] * a.scale, acc_dq[db][4 * jj + 1] * a.scale,
                 acc_dq[db][4 * jj + 2] * a.scale, acc_dq[db][4 * jj + 3] * a.scale};
 }
@@ -307,12 +328,15 @@ __global__ __launch_bounds__(kThreadsB) void bwd_dq(BwdArgs a) {
 template <int D>
 __global__ __launch_bounds__(kThreadsB) void bwd_dkdv(BwdArgs a) {
   constexpr int BQ = kStepB;
-  constexpr int KC = D / 16, DB = D / 32, QB = BQ / 32;
+  constexpr int KC = D / 16, DB = kCols<D> / 32, QB = BQ / 32;
   using TL = TileLayout<D>;
   __shared__ SmemTiles<D> sm;
 
   Item it;
-  if (!decode_item(a, __builtin_amdgcn_workgroup_id_x(), 0, it)) return;
+  int half;
+  const int bid = split_index<D>(__builtin_amdgcn_workgroup_id_x(), half);
+  const int c0 = half * kCols<D>;  // first head-dim column this item accumulates
+  if (!decode_item(a, bid, 0, it)) return;
   const BwdPat& P = a.pat[it.pi];
   const int kt_idx = P.ntiles - 1 - it.tq;  // longest (first) key tiles first
   const int L = it.L;
@@ -369,7 +393,7 @@ __global__ __launch_bounds__(kThreadsB) void bwd_dkdv(BwdArgs a) {
   for (int db = 0; db < DB; ++db)
 #pragma unroll
     for (int t = 0; t < 2; ++t) {
-      const int d = db * 32 + tr_d;
+      const int d = c0 + db * 32 + tr_d;
       vtr_off[db][t] = TL::offset(8 * t + 4 * hi + tr_r, d >> 3) + (d & 7) * 2;
     }
 
@@ -473,7 +497,7 @@ __global__ __launch_bounds__(kThreadsB) void bwd_dkdv(BwdArgs a) {
   for (int db = 0; db < DB; ++db)
 #pragma unroll
     for (int jj = 0; jj < 4; ++jj) {
-      const int d = db * 32 + 8 * jj + 4 * hi;
+      const int d = c0 + db * 32 + 8 * jj + 4 * hi;
       *reinterpret_cast<f32x4*>(krow_out + d) =
           f32x4{acc_dk[db][4 * jj] * a.scale, acc_dk[db][4 * jj + 1] * a.scale, acc_dk[db][4 * jj + 2] * a.scale,
                 acc_dk[db][4 * jj + 3] * a.scale};
@@ -614,6 +638,7 @@ hipError_t launch_backward(const Plan& plan, const BwdLayout& lay, const void* q
   }
   const dim3 rgrid(static_cast<unsigned>(rblocks));
   const dim3 igrid(static_cast<unsigned>(plan.launch_items));
+  if (2 * plan.launch_items >= (int64_t{1} << 31)) return hipErrorInvalidValue;
   switch (plan.D) {
     case 32:
       hipLaunchKernelGGL(bwd_delta<32>, rgrid, dim3(kThreadsB), 0, stream, da_);
@@ -631,6 +656,16 @@ hipError_t launch_backward(const Plan& plan, const BwdLayout& lay, const void* q
       }
       hipLaunchKernelGGL(bwd_sum<64>, rgrid, dim3(kThreadsB), 0, stream, sa);
       break;
+    case 128: {
+      const dim3 igrid2(static_cast<unsigned>(2 * plan.launch_items));
+      hipLaunchKernelGGL(bwd_delta<128>, rgrid, dim3(kThreadsB), 0, stream, da_);
+      if (plan.total_items > 0) {
+        hipLaunchKernelGGL(bwd_dq<128>, igrid2, dim3(kThreadsB), 0, stream, a);
+        hipLaunchKernelGGL(bwd_dkdv<128>, igrid2, dim3(kThreadsB), 0, stream, a);
+      }
+      hipLaunchKernelGGL(bwd_sum<128>, rgrid, dim3(kThreadsB), 0, stream, sa);
+      break;
+    }
     default:
       return hipErrorInvalidValue;
   }

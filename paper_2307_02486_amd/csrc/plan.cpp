@@ -128,7 +128,7 @@ int make_plan(int64_t B, int64_t N, int64_t H, int64_t D, const da_pattern_t* pa
 
 int make_bwd_layout(const Plan& p, BwdLayout* out) {
   if (!out) return DA_EINVAL;
-  if (p.dtype != DA_BF16 || (p.D != 32 && p.D != 64)) return DA_EUNSUPPORTED;
+  if (p.dtype != DA_BF16) return DA_EUNSUPPORTED;
   // 32-bit offsets inside a tile of 64 kept rows (rows r*H*D elements apart,
   // and the rows' per-row scalars r floats apart)
   if (!p.offsets32) return DA_EUNSUPPORTED;

@@ -80,7 +80,7 @@ struct BwdLayout {
 };
 
 // Backward workspace and work of a validated forward plan.  DA_EUNSUPPORTED
-// unless the plan is bf16 with D in {32, 64}.
+// unless the plan is bf16 (and for tiles whose offsets need 64 bits).
 int make_bwd_layout(const Plan& p, BwdLayout* out);
 
 // Query rows per work item of the attention kernel for a dtype.

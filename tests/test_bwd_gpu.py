@@ -55,6 +55,8 @@ CASES = [
     (1, 200, 5, 32, [(50, 3)], True),                    # rows no pattern keeps: zero gradients
     (1, 1031, 6, 64, [(2048, 1), (4096, 3), (333, 2)], True),  # w > N
     (1, 64, 16, 64, [(64, 64), (64, 1)], True),          # r = w
+    (1, 513, 17, 128, [(512, 1), (513, 20)], True),      # D = 128 (two column halves)
+    (2, 777, 3, 128, [(256, 1), (512, 7), (1000, 9)], False),
 ]
 
 
@@ -126,3 +128,30 @@ def test_backward_error_leaves_buffers_untouched():
         dilated_attn_bwd(q, k, v, out, lse, dout, [(64, 1)], True, dq=dq, workspace=small)
     torch.cuda.synchronize()
     assert (dq == 7.0).all()
+
+
+def test_backward_n1m_sampled_rows():
+    """The 1M-token, D = 128 workload (six patterns up to w = N): dq on random
+    rows, dk and dv on rows at the end of the sequence (the queries seeing a
+    key there are few, which keeps the oracle cheap), heads 0 and 15."""
+    wl = workloads.BY_NAME["n1m_h16_d128_6pat"]
+    note("[bwd] n1m sampled rows")
+    q, k, v = workloads.make_qkv(wl, device="cuda")
+    dout = workloads.make_random(q.shape, torch.bfloat16, 1.0, wl.seed, "cuda", 3)
+    pats = list(wl.patterns)
+    dq, dk, dv = _gpu_bwd(q, k, v, dout, pats, wl.causal)
+    for t in (dq, dk, dv):
+        assert torch.isfinite(t).all().item()
+    rng = np.random.default_rng(9)
+    qrows = [(0, int(p), h) for h in (0, 15) for p in sorted(set(rng.integers(0, wl.N, 8).tolist()) | {0, wl.N - 1})]
+    krows = [(0, wl.N - 1 - i, h) for h in (0, 15) for i in range(0, 64, 9)]
+    qc, kc, vc, oc = q.cpu(), k.cpu(), v.cpu(), dout.cpu()
+    rq = oracle.dq_rows_ref(qc, kc, vc, oc, pats, True, None, qrows)
+    rk, rv = oracle.dkdv_rows_ref(qc, kc, vc, oc, pats, True, None, krows)
+    def pick(t, rows):
+        return t[tuple(torch.tensor([r[i] for r in rows]) for i in range(3))].double().numpy()
+    e = _check("dq", pick(dq.cpu(), qrows), rq, "n1m")
+    note(f"[bwd] n1m dq: {len(qrows)} rows, err {e:.2e}")
+    for n, g, r in (("dk", dk, rk), ("dv", dv, rv)):
+        e = _check(n, pick(g.cpu(), krows), r, "n1m")
+        note(f"[bwd] n1m {n}: {len(krows)} rows, err {e:.2e}")

@@ -181,14 +181,16 @@ def test_bwd_plan_accounting():
 
 
 def test_bwd_unsupported_and_errors(lib):
-    """The backward covers bf16 with D in {32, 64}; argument errors return
+    """The backward covers bf16 (D in {32, 64, 128}); argument errors return
     before any HIP call (fake, never dereferenced pointers)."""
     from paper_2307_02486_amd import _lib, plan_raw
     arr, n = _lib.pattern_array([(8, 1)])
     info = _lib.PlanInfo()
     import ctypes
-    assert _lib.ERRORS[lib.dilated_attn_bwd_plan(1, 16, 2, 128, arr, n, 1, 1, 0.0, ctypes.byref(info))] == \
-        "DA_EUNSUPPORTED"
+    assert lib.dilated_attn_bwd_plan(1, 16, 2, 128, arr, n, 1, 1, 0.0, ctypes.byref(info)) == 0
+    huge, hn = _lib.pattern_array([(1 << 20, 1 << 19)])      # a 65-row tile spans > 2 GiB
+    assert _lib.ERRORS[lib.dilated_attn_bwd_plan(1, 1 << 20, 64, 128, huge, hn, 1, 1, 0.0,
+                                                 ctypes.byref(info))] == "DA_EUNSUPPORTED"
     assert _lib.ERRORS[lib.dilated_attn_bwd_plan(1, 16, 2, 64, arr, n, 1, 0, 0.0, ctypes.byref(info))] == \
         "DA_EUNSUPPORTED"
     assert lib.dilated_attn_bwd_plan(1, 16, 2, 64, arr, n, 1, 1, 0.0, ctypes.byref(info)) == 0
@@ -203,5 +205,5 @@ def test_bwd_unsupported_and_errors(lib):
     assert _lib.ERRORS[call(good[:6] + [good[0]] + good[7:])] == "DA_EINVAL"     # dq aliases q
     assert _lib.ERRORS[call(good[:7] + [good[6]] + good[8:])] == "DA_EINVAL"     # dk aliases dq
     assert _lib.ERRORS[call(good, ws=good[5])] == "DA_EINVAL"                     # workspace aliases dout
-    assert _lib.ERRORS[call(good, D=128)] == "DA_EUNSUPPORTED"
+    assert _lib.ERRORS[call(good, D=40)] == "DA_EUNSUPPORTED"
     assert _lib.ERRORS[call(good, dtype=0)] == "DA_EUNSUPPORTED"
