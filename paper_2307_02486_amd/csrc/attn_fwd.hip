@@ -47,15 +47,26 @@ constexpr int kBM = 128;       // query rows per work item
 #define DA_KEY_TILE 64
 #endif
 constexpr int kBN = DA_KEY_TILE;  // keys per K/V tile
-// A row's running max is raised only when a tile's max exceeds it by more than
-// this (log2 units); until then probabilities may reach 2^kRescaleSlack, which
-// bf16 and the fp32 sums hold exactly as well as values below 1.
+// Online softmax without a per-tile row max.  Each row's reference max m is
+// the true max of its first key tile; later tiles exponentiate S - m directly
+// and the row's reference is moved only afterwards, from the tile's row sums:
+// a tile whose probabilities of one half-row sum to more than kSumSlack moves
+// m up by log2 of the row's tile sum (so that the tile's probabilities, and
+// the output accumulated so far, are rescaled to a sum of one).  Probabilities
+// above 1 are held by bf16 and the fp32 sums exactly as well as those below.
+// A half-row sum above kSumLimit (or not finite: a probability overflowed)
+// makes the whole work item run again in the safe mode, which takes the row
+// max of every tile before exponentiating (raising m when the tile max exceeds
+// it by more than kRescaleSlack).
 constexpr float kRescaleSlack = 8.0f;
+constexpr float kSumSlack = 1024.0f;
+constexpr float kSumLimit = 4294967296.0f;  // 2^32
 
 template <int D>
 struct SmemBf16 {
   __attribute__((aligned(16))) u16 k[2][kBN * D];  // double-buffered K tiles
   __attribute__((aligned(16))) u16 v[2][kBN * D];  // double-buffered V tiles
+  int redo;  // set by a wave whose tile sums left the fast path's range
 };
 
 template <int D, bool kBufferLoads>
@@ -150,13 +161,6 @@ __global__ __launch_bounds__(kThreads) void attn_fwd_bf16(AttnArgs a) {
     }
   };
 
-  f32x16 acc_o[DB];
-#pragma unroll
-  for (int db = 0; db < DB; ++db) acc_o[db] = f32x16{};
-  float m_run = 0.0f;     // reference max of scaled scores (log2 domain), set by tile 0
-  f32x16 negm = f32x16{}; // -m_run in every slot: the initial value of each S' block
-  float l_run = 0.0f;     // this half-wave's share of the running denominator
-
   const int kv_end = a.causal ? qend : L;
   const int ntile = (kv_end + BN - 1) / BN;
   const int wq_lo = q0 + wv * 32;  // smallest query of this wave
@@ -186,6 +190,18 @@ __global__ __launch_bounds__(kThreads) void attn_fwd_bf16(AttnArgs a) {
       const unsigned bits = q_valid ? (qraw[c][e >> 1] >> (16 * (e & 1))) << 16 : 0u;
       qreg[c][e] = (__bf16)(__builtin_bit_cast(float, bits) * a.scale_log2);
     }
+  if (tid == 0) sm.redo = 0;
+
+  f32x16 acc_o[DB];
+  float m_run, l_run;  // reference max (log2 domain) and this half-wave's share of the denominator
+  f32x16 negm;         // -m_run in every slot: the initial value of each S' block
+  bool safe = false;   // safe mode: a row max for every tile
+  for (;;) {
+#pragma unroll
+  for (int db = 0; db < DB; ++db) acc_o[db] = f32x16{};
+  m_run = 0.0f;
+  l_run = 0.0f;
+  negm = f32x16{};
   __builtin_amdgcn_s_waitcnt(kWaitVmcnt0);
   __syncthreads();
   for (int jt = 0; jt < ntile; ++jt) {
@@ -229,31 +245,34 @@ __global__ __launch_bounds__(kThreads) void attn_fwd_bf16(AttnArgs a) {
           for (int j = 0; j < 16; ++j)
             if (base + kb * 32 + 8 * (j >> 2) + (j & 3) > 0) acc_s[kb][j] = -INFINITY;
       }
-      // Tile max of this lane's query, across both half-waves.
-      float mx = -INFINITY;
-#pragma unroll
-      for (int kb = 0; kb < SB; ++kb)
-#pragma unroll
-        for (int j = 0; j < 16; j += 2) mx = fmaxf(mx, fmaxf(acc_s[kb][j], acc_s[kb][j + 1]));
-      mx = fmaxf(mx, other_half(mx));  // already relative to m_run, log2 units
-      // Lazy rescale: the first tile fixes the reference max; later tiles move
-      // it only when some row of the wave would see probabilities above
-      // 2^kRescaleSlack.
-      if (jt == 0 || __any(mx > kRescaleSlack)) {
-        const float delta = jt == 0 ? mx : fmaxf(mx, 0.0f);
-        const float alpha = __builtin_amdgcn_exp2f(-delta);
-        m_run += delta;
-        l_run *= alpha;
-#pragma unroll
-        for (int db = 0; db < DB; ++db)
-#pragma unroll
-          for (int j = 0; j < 16; ++j) acc_o[db][j] *= alpha;
+      // The first tile (and every tile in the safe mode) takes the row max of
+      // this lane's query, across both half-waves.
+      if (jt == 0 || safe) {
+        float mx = -INFINITY;
 #pragma unroll
         for (int kb = 0; kb < SB; ++kb)
 #pragma unroll
-          for (int j = 0; j < 16; ++j) acc_s[kb][j] -= delta;
+          for (int j = 0; j < 16; j += 2) mx = fmaxf(mx, fmaxf(acc_s[kb][j], acc_s[kb][j + 1]));
+        mx = fmaxf(mx, other_half(mx));  // already relative to m_run, log2 units
+        // The first tile fixes the reference max; in the safe mode later tiles
+        // move it only when some row of the wave would see probabilities above
+        // 2^kRescaleSlack.
+        if (jt == 0 || __any(mx > kRescaleSlack)) {
+          const float delta = jt == 0 ? mx : fmaxf(mx, 0.0f);
+          const float alpha = __builtin_amdgcn_exp2f(-delta);
+          m_run += delta;
+          l_run *= alpha;
 #pragma unroll
-        for (int j = 0; j < 16; ++j) negm[j] = -m_run;
+          for (int db = 0; db < DB; ++db)
+#pragma unroll
+            for (int j = 0; j < 16; ++j) acc_o[db][j] *= alpha;
+#pragma unroll
+          for (int kb = 0; kb < SB; ++kb)
+#pragma unroll
+            for (int j = 0; j < 16; ++j) acc_s[kb][j] -= delta;
+#pragma unroll
+          for (int j = 0; j < 16; ++j) negm[j] = -m_run;
+        }
       }
       // P = exp2(S'); bf16 P feeds the PV MFMA.  Row sums are taken in fp32
       // with plain adds (dot-product instructions would not issue while other
@@ -297,12 +316,40 @@ __global__ __launch_bounds__(kThreads) void attn_fwd_bf16(AttnArgs a) {
           }
         });
       });
-      l_run += (lp[0] + lp[1]) + (lp[2] + lp[3]);
+      const float lt = (lp[0] + lp[1]) + (lp[2] + lp[3]);
+      l_run += lt;
+      // Fast mode: move the reference max after the fact when this tile's
+      // probabilities grew large (rare), or ask for a safe rerun when they
+      // could have overflowed.
+      if (!safe && __any(!(lt <= kSumSlack))) {
+        if (__any(!(lt <= kSumLimit))) {
+          sm.redo = 1;
+        } else {
+          const float lc = lt + other_half(lt);
+          const float delta = lc > 1.0f ? __builtin_amdgcn_logf(lc) : 0.0f;  // log2
+          const float alpha = __builtin_amdgcn_exp2f(-delta);
+          m_run += delta;
+          l_run *= alpha;
+#pragma unroll
+          for (int db = 0; db < DB; ++db)
+#pragma unroll
+            for (int j = 0; j < 16; ++j) acc_o[db][j] *= alpha;
+#pragma unroll
+          for (int j = 0; j < 16; ++j) negm[j] = -m_run;
+        }
+      }
     }
     // The next tile's loads have landed in LDS and every wave is done with
     // this tile before anyone moves on.
     __builtin_amdgcn_s_waitcnt(kWaitVmcnt0);
     __syncthreads();
+  }
+  // A wave that saw a tile sum beyond kSumLimit makes the whole workgroup run
+  // the item again (uniformly: the flag is read after the last barrier).
+  if (safe || __builtin_amdgcn_readfirstlane(sm.redo) == 0) break;
+  safe = true;
+  __syncthreads();  // every wave has read the flag before the tiles are reloaded
+  load_tile(0, 0);
   }
 
   // Epilogue: normalise this wave's 32 rows of the per-pattern output and

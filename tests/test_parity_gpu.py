@@ -91,6 +91,55 @@ def test_edge_cases(case):
     compare_full(q, k, v, pats, causal, dt, tag=str(case))
 
 
+# ---- online-softmax regimes: scores that grow along the sequence --------------
+
+LOG2E = 1.4426950408889634
+
+
+def _integer_qkv(B, N, H, D, seed, jump_at, jump):
+    """q, k with small integer entries (exact in bf16) and keys from position
+    `jump_at` on multiplied by `jump`; v ~ N(0, 1) in bf16.  With the scale
+    2^-3 / log2(e) the kernel's scaled scores (log2 units) are q.k / 8 exactly."""
+    g = torch.Generator().manual_seed(seed)
+    q = torch.randint(-2, 3, (B, N, H, D), generator=g).to(torch.float32)
+    k = torch.randint(-2, 3, (B, N, H, D), generator=g).to(torch.float32)
+    k[:, jump_at:] *= jump
+    v = torch.randn((B, N, H, D), generator=g)
+    return (x.to(torch.bfloat16).cuda() for x in (q, k, v))
+
+
+def _max_excess(q, k, causal, tile=64):
+    """Largest amount (log2 units) by which a visible score of a query exceeds
+    the max over the visible keys of the first 64-key tile, dense pattern."""
+    qf, kf = q[0, :, 0].float().cpu(), k[0, :, 0].float().cpu()
+    s = (qf @ kf.T) / 8.0
+    N = s.shape[0]
+    if causal:
+        s = s.masked_fill(torch.ones(N, N, dtype=torch.bool).triu(1), float("-inf"))
+    first = s[:, :tile].max(dim=1).values
+    return float((s.max(dim=1).values - first).max())
+
+
+@pytest.mark.parametrize("D", [64, 128])
+@pytest.mark.parametrize("causal", [True, False])
+@pytest.mark.parametrize("regime,jump,lo,hi", [("rescale", 2.0, 10.0, 26.0), ("rerun", 8.0, 40.0, 120.0),
+                                               ("overflow", 16.0, 140.0, 1e9)])
+def test_growing_scores(D, causal, regime, jump, lo, hi):
+    """Later keys score far above the first key tile.  'rescale': the
+    reference max is moved after a tile (tile sums above the slack, below the
+    limit); 'rerun': tile sums pass the limit, so the work item runs again
+    with a row max for every tile; 'overflow': probabilities overflow to
+    infinity before that rerun.  All must match the oracle."""
+    B, N, H = 1, 1000, 2
+    note(f"[softmax regime] {regime} D={D} causal={causal}")
+    q, k, v = _integer_qkv(B, N, H, D, seed=31 + D, jump_at=300, jump=jump)
+    ex = _max_excess(q, k, causal)
+    assert lo <= ex <= hi, f"construction gives a max excess of {ex} (wanted [{lo}, {hi}])"
+    scale = 0.125 / LOG2E
+    eo, el = compare_full(q, k, v, [(1000, 1), (500, 2)], causal, "bf16", scale=scale, tag=f"{regime} D{D}")
+    note(f"[softmax regime] {regime}: excess {ex:.1f}, out err {eo:.3e} lse err {el:.3e}")
+
+
 @pytest.mark.parametrize("dt", ["bf16", "f32"])
 def test_q_zero_closed_form(dt):
     """q = 0: lse = ln(count of visible keys over all patterns), out = their mean."""
