@@ -1,17 +1,21 @@
 """Benchmark of the dilated-attention forward pass on one MI355X.
 
-One step = one dilated_attn_fwd call (attention stage + combine stage) over
-the N=32768, H=12, D=64 bf16 workload with the five patterns
-(2048,1) (4096,2) (8192,4) (16384,6) (32768,12), inputs resident in HBM.
+One step = one dilated_attn_fwd call over the N=32768, H=12, D=64 bf16
+workload with the five patterns (2048,1) (4096,2) (8192,4) (16384,6)
+(32768,12), inputs resident in HBM.  With bf16 inputs and an r = 1 pattern the
+call is two launches of the attention kernel: every other pattern, then the
+r = 1 pattern with the combine fused into its epilogue.
 
 Prints one JSON line: effective TFLOP/s over the exact sparse flops (4*D per
-unmasked query-key pair) and tokens/s of the timed back-to-back steps, per-stage
-times from a second pass in which the library records HIP events around each
-of its kernels on the call's stream, the attention stage's MFMA
-roofline fraction, and the CPU oracle timed on a bounded sample on this host.
-After the timed region, a second pass times each step on its own (median,
-minimum, mean), once as is and once with a 512 MiB buffer written before each
-step so that the inputs are no longer held in the Infinity Cache.
+unmasked query-key pair) and tokens/s of the timed back-to-back steps, the
+times of the call's two launches from a second pass in which the library
+records HIP events around them on the call's stream, the attention kernel's
+MFMA roofline fraction, the same figures for the path with a separate combine
+kernel (DILATED_ATTN_SEPARATE_COMBINE=1) including that kernel's HBM
+bandwidth, and the CPU oracle timed on a bounded sample on this host.  After
+the timed region, a further pass times each step on its own (median, minimum,
+mean), once as is and once with a 512 MiB buffer written before each step so
+that the inputs are no longer held in the Infinity Cache.
 """
 from __future__ import annotations
 
@@ -294,36 +298,61 @@ def main():
     def step():
         dilated_attn(q, k, v, pats, wl.causal, out=out, lse=lse, workspace=ws, stream=stream)
 
-    for _ in range(args.warmup):
-        step()
-    torch.cuda.synchronize()
-    t_start = torch.cuda.Event(enable_timing=True)
-    t_end = torch.cuda.Event(enable_timing=True)
-    # Timed region: exactly `steps` back-to-back calls, nothing else on the stream.
-    torch.cuda.synchronize()
-    t_start.record(stream)
-    for _ in range(args.steps):
-        step()
-    t_end.record(stream)
-    torch.cuda.synchronize()
-    total_ms = t_start.elapsed_time(t_end)
-    ms = total_ms / args.steps
-    # Per-stage split: the same number of calls again, with the library recording
-    # HIP events around each of its two kernels on the call's stream.
-    with StageTimer(capacity=max(1, args.steps)) as st:
-        for _ in range(args.steps):
+    def timed(steps):
+        """Mean ms per call over `steps` back-to-back calls, then the mean ms
+        of the call's two launches over as many calls again."""
+        for _ in range(args.warmup):
             step()
         torch.cuda.synchronize()
-    ms_attn = st.ms_attention / max(1, st.calls)
-    ms_comb = st.ms_combine / max(1, st.calls)
+        t_start = torch.cuda.Event(enable_timing=True)
+        t_end = torch.cuda.Event(enable_timing=True)
+        # Timed region: exactly `steps` back-to-back calls, nothing else on the stream.
+        t_start.record(stream)
+        for _ in range(steps):
+            step()
+        t_end.record(stream)
+        torch.cuda.synchronize()
+        ms = t_start.elapsed_time(t_end) / steps
+        # The library records HIP events around its two launches on the call's stream.
+        with StageTimer(capacity=max(1, steps)) as st:
+            for _ in range(steps):
+                step()
+            torch.cuda.synchronize()
+        return ms, st.ms_attention / max(1, st.calls), st.ms_combine / max(1, st.calls)
+
     flops = info["sparse_flops"]
-    tflops = flops / (ms * 1e-3) / 1e12
-    attn_tflops = flops / (ms_attn * 1e-3) / 1e12
-    comb_gbs = info["bytes_combine"] / (ms_comb * 1e-3) / 1e9
     peak = PEAK_BF16_TFLOPS if wl.dtype == "bf16" else PEAK_F32_TFLOPS
+    fused = bool(info["combine_fused"])
+    separate = None
+    if fused:
+        # The path with a separate combine kernel, for that kernel's bandwidth.
+        os.environ["DILATED_ATTN_SEPARATE_COMBINE"] = "1"
+        try:
+            s_ms, s_attn, s_comb = timed(args.steps)
+        finally:
+            del os.environ["DILATED_ATTN_SEPARATE_COMBINE"]
+        s_gbs = info["bytes_combine"] / (s_comb * 1e-3) / 1e9
+        s_tf = flops / (s_attn * 1e-3) / 1e12
+        separate = {"ms_per_step": round(s_ms, 5), "tflops": round(flops / (s_ms * 1e-3) / 1e12, 3),
+                    "attention_ms": round(s_attn, 5), "attention_tflops": round(s_tf, 3),
+                    "attention_frac_of_mfma_peak": round(s_tf / peak, 4),
+                    "combine_ms": round(s_comb, 5), "combine_algorithmic_bytes": info["bytes_combine"],
+                    "combine_gbps": round(s_gbs, 1), "combine_frac_of_hbm_peak": round(s_gbs / PEAK_HBM_GBS, 4)}
+    ms, ms_first, ms_second = timed(args.steps)
+    tflops = flops / (ms * 1e-3) / 1e12
     prof = profiled_counters(wl.name)
-    traffic = prof.get("attention_bytes_per_launch")
-    comb_traffic = prof.get("combine_bytes_per_launch")
+    if fused:
+        # Both launches run the attention kernel; the second also mixes the patterns.
+        ms_attn = ms_first + ms_second
+        traffic = prof.get("fused_attention_bytes_per_call")
+        stages = {"launch_other_patterns_ms": round(ms_first, 5),
+                  "launch_fused_pattern_with_combine_ms": round(ms_second, 5)}
+    else:
+        ms_attn = ms_first
+        traffic = prof.get("attention_bytes_per_launch")
+        stages = {"attention_ms": round(ms_first, 5), "combine_ms": round(ms_second, 5)}
+    attn_tflops = flops / (ms_attn * 1e-3) / 1e12
+    comb_gbs = info["bytes_combine"] / (ms_second * 1e-3) / 1e9
     res = {
         "metric": METRIC,
         "value": round(tflops, 3),
@@ -340,12 +369,16 @@ def main():
         "config": wl.describe(),
         "tokens_per_s": round(wl.B * wl.N / (ms * 1e-3), 1),
         "sparse_flops": flops,
+        "combine_fused": fused,
+        "launches": stages,
         "attention_stage": {"ms": round(ms_attn, 5), "tflops": round(attn_tflops, 3),
                             "frac_of_mfma_peak": round(attn_tflops / peak, 4),
                             "mfma_busy_pct_profiled": prof.get("attention_mfma_busy_pct")},
-        "combine_stage": {"ms": round(ms_comb, 5), "algorithmic_bytes": info["bytes_combine"],
-                          "gbps": round(comb_gbs, 1), "frac_of_hbm_peak": round(comb_gbs / PEAK_HBM_GBS, 4),
-                          "traffic": comb_traffic},
+        "combine_stage": ({"fused_into_attention": True} if fused else
+                          {"ms": round(ms_second, 5), "algorithmic_bytes": info["bytes_combine"],
+                           "gbps": round(comb_gbs, 1), "frac_of_hbm_peak": round(comb_gbs / PEAK_HBM_GBS, 4),
+                           "traffic": prof.get("combine_bytes_per_launch")}),
+        "separate_combine_path": separate,
         "roofline": {"bound": "mfma", "achieved": round(attn_tflops, 3), "peak": peak,
                      "unit": "TFLOP/s", "frac": round(attn_tflops / peak, 4), "traffic": traffic},
         "cpu_baseline": None,

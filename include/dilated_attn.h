@@ -76,6 +76,12 @@ typedef struct {
   double bytes_combine;     /* algorithmic HBM bytes of the combine stage:
                                per-pattern output and lse read once, out and
                                lse written once                               */
+  int64_t combine_fused;    /* 1: fwd runs the combine inside the attention
+                               kernel of the first pattern with r = 1 (bf16
+                               inputs and D <= 64, unless the environment
+                               variable DILATED_ATTN_SEPARATE_COMBINE is "1"),
+                               as a second attention launch after the other
+                               patterns'; 0: a separate combine kernel       */
 } da_plan_info_t;
 
 /*
@@ -185,9 +191,12 @@ const char* dilated_attn_strerror(int code);
  *
  * dilated_attn_profile_begin(capacity) creates 3*capacity HIP events on the
  * current device; each of the next `capacity` dilated_attn_fwd calls records
- * one event before the attention stage, one between the stages and one after
- * the combine stage, on the call's stream (calls beyond capacity are not
- * timed).  dilated_attn_profile_end waits for the recorded events, writes the
+ * one event before its first launch, one between its two launches and one
+ * after the second, on the call's stream (calls beyond capacity are not
+ * timed).  The two launches are the attention stage and the combine stage,
+ * or, with the combine fused (da_plan_info_t.combine_fused), the attention
+ * launch of every pattern but the fused one and the attention launch of the
+ * fused pattern with the combine.  dilated_attn_profile_end waits for the recorded events, writes the
  * summed durations of the two stages in milliseconds and the number of timed
  * calls, and destroys the events.  capacity must be in [1, 1<<20]; any
  * pointer argument of profile_end may be NULL.  Not thread safe: one profiling

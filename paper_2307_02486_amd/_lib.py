@@ -31,7 +31,8 @@ class PlanInfo(ctypes.Structure):
                 ("covered_rows", ctypes.c_int64),
                 ("sparse_flops", ctypes.c_double),
                 ("bytes_attn", ctypes.c_double),
-                ("bytes_combine", ctypes.c_double)]
+                ("bytes_combine", ctypes.c_double),
+                ("combine_fused", ctypes.c_int64)]
 
 
 class DilatedAttnError(RuntimeError):

@@ -32,8 +32,6 @@
 namespace da {
 namespace {
 
-typedef float f32x8 __attribute__((ext_vector_type(8)));
-
 struct BwdPat {
   int32_t w, r, nseg, lmax, ntiles, units;
   int64_t dq_off, dk_off, dv_off;  // byte offsets of the compact float32 gradients

@@ -33,9 +33,15 @@ struct AttnArgs {
   char* ws;
   int32_t B, N, H, npat, causal, total_items;
   float scale_log2;  // softmax scale times log2(e): scores go to exp2 directly
-  // The patterns, ordered by query tiles per unit, most first (the kernels
-  // only use a pattern's index to find its record here).
+  // The patterns of this launch, ordered by query tiles per unit, most first
+  // (the kernels only use a pattern's index to find its record here).
   PatArgs pat[DA_MAX_PATTERNS];
+  // Fused combine only: out, lse and every pattern of the call in the call's
+  // order; mix[fuse] is the pattern this launch computes.
+  void* out;
+  float* lse;
+  int32_t mix_npat, fuse;
+  MixPat mix[DA_MAX_PATTERNS];
 };
 
 // ---------------------------------------------------------------------------
@@ -69,7 +75,11 @@ struct SmemBf16 {
   int redo;  // set by a wave whose tile sums left the fast path's range
 };
 
-template <int D, bool kBufferLoads>
+// kMixNP = 0: the per-pattern rows go to the workspace.  kMixNP > 0: this
+// launch computes a pattern with r = 1 after every other pattern's rows are
+// in the workspace, and its epilogue mixes them (kMixNP >= the call's pattern
+// count bounds the mixing loops at compile time).
+template <int D, bool kBufferLoads, int kMixNP>
 __global__ __launch_bounds__(kThreads) void attn_fwd_bf16(AttnArgs a) {
   static_assert(D % 32 == 0, "head dim must be a multiple of 32");
   constexpr int BN = kBN;
@@ -373,18 +383,97 @@ __global__ __launch_bounds__(kThreads) void attn_fwd_bf16(AttnArgs a) {
       for (int e = 0; e < 4; ++e) o[e] = (_Float16)(acc_o[db][4 * jj + e] * inv);
       *reinterpret_cast<f16x4*>(stg + stg_off(qr, db * 4 + jj) + 8 * hi) = o;
     }
-  if (hi == 0 && q_valid)
-    reinterpret_cast<float*>(a.ws + P.lse_off)[(int64_t)it.unit * P.lmax + tq_row] =
-        (m_run + __builtin_amdgcn_logf(l_tot)) * kLn2;
-  // Each pass writes 64 consecutive 16-byte chunks: 1024 / (2 D) rows.
+  const float lse_own = (m_run + __builtin_amdgcn_logf(l_tot)) * kLn2;
+  // Each pass covers 64 consecutive 16-byte chunks: 1024 / (2 D) rows.
   constexpr int kPasses = 32 * TL::kRowBytes / 1024;
-  _Float16* obase = reinterpret_cast<_Float16*>(a.ws + P.o_off) + ((int64_t)it.unit * P.lmax + wq_lo) * D;
+  if constexpr (kMixNP == 0) {
+    if (hi == 0 && q_valid)
+      reinterpret_cast<float*>(a.ws + P.lse_off)[(int64_t)it.unit * P.lmax + tq_row] = lse_own;
+    _Float16* obase = reinterpret_cast<_Float16*>(a.ws + P.o_off) + ((int64_t)it.unit * P.lmax + wq_lo) * D;
 #pragma unroll
-  for (int i = 0; i < kPasses; ++i) {
-    const int row = (i * 64 + lane) / TL::kSlots;
-    const int chunk = (i * 64 + lane) % TL::kSlots;
-    const u32x4 x = *reinterpret_cast<const u32x4*>(stg + stg_off(row, chunk));
-    if (wq_lo + row < L) *reinterpret_cast<u32x4*>(obase + row * D + chunk * 8) = x;
+    for (int i = 0; i < kPasses; ++i) {
+      const int row = (i * 64 + lane) / TL::kSlots;
+      const int chunk = (i * 64 + lane) % TL::kSlots;
+      const u32x4 x = *reinterpret_cast<const u32x4*>(stg + stg_off(row, chunk));
+      if (wq_lo + row < L) *reinterpret_cast<u32x4*>(obase + row * D + chunk * 8) = x;
+    }
+  } else {
+    // Fused combine (Sec. 2.2, Eqs. 7-10).  This pattern has r = 1, so kept
+    // row t of the segment is position p0 + t and every position of the
+    // sequence is some item's row.  Each lane takes 16-byte chunks of the
+    // wave's staged rows, loads the same chunk of every other pattern that
+    // keeps the position (with its lse) from the workspace, and mixes them
+    // exactly as the separate combine kernel does, in the call's pattern
+    // order: the two paths give identical results.
+    float* lse_stg = reinterpret_cast<float*>(&sm.v[0][0]) + wv * 32;
+    if (hi == 0) lse_stg[qr] = lse_own;
+    constexpr int NP = kMixNP;
+    constexpr int PG = NP >= 16 ? 1 : 16 / NP;  // passes whose loads are in flight together
+    const int64_t bh = (int64_t)it.b * a.H + it.h;
+#pragma unroll
+    for (int i0 = 0; i0 < kPasses; i0 += PG) {
+      f16x8 ow[PG][NP];
+      float lw[PG][NP];
+#pragma unroll
+      for (int ip = 0; ip < PG; ++ip) {
+        const int i = i0 + ip;
+        const int row = (i * 64 + lane) / TL::kSlots;
+        const int chunk = (i * 64 + lane) % TL::kSlots;
+        const uint32_t p = static_cast<uint32_t>(it.p0 + wq_lo + row);
+        const bool valid = i < kPasses && wq_lo + row < L;
+#pragma unroll
+        for (int j = 0; j < NP; ++j) {
+          lw[ip][j] = -INFINITY;
+          if (j >= a.mix_npat || j == a.fuse || !valid) continue;
+          const MixPat& M = a.mix[j];
+          const uint32_t g = M.fw.div(p);
+          const uint32_t pos = p - g * M.fw.d;
+          const uint32_t t = M.fr.div(pos);
+          const uint32_t sj = static_cast<uint32_t>(it.h) - M.fr.div(static_cast<uint32_t>(it.h)) * M.fr.d;
+          if (pos - t * M.fr.d != sj) continue;
+          const int64_t wrow = (bh * M.nseg + g) * M.lmax + t;
+          lw[ip][j] = __builtin_nontemporal_load(reinterpret_cast<const float*>(a.ws + M.lse_off) + wrow);
+          ow[ip][j] = __builtin_nontemporal_load(
+              reinterpret_cast<const f16x8*>(reinterpret_cast<const _Float16*>(a.ws + M.o_off) + wrow * D + chunk * 8));
+        }
+      }
+#pragma unroll
+      for (int ip = 0; ip < PG; ++ip) {
+        const int i = i0 + ip;
+        const int row = (i * 64 + lane) / TL::kSlots;
+        const int chunk = (i * 64 + lane) % TL::kSlots;
+        if (!(i < kPasses && wq_lo + row < L)) continue;
+        const int p = it.p0 + wq_lo + row;
+        const f16x8 own = *reinterpret_cast<const f16x8*>(stg + stg_off(row, chunk));
+        const float l0 = lse_stg[row];
+        float m = -INFINITY;
+#pragma unroll
+        for (int j = 0; j < NP; ++j) m = fmaxf(m, j == a.fuse ? l0 : lw[ip][j]);
+        float den = 0.0f;
+        f32x8 acc = f32x8{0, 0, 0, 0, 0, 0, 0, 0};
+#pragma unroll
+        for (int j = 0; j < NP; ++j) {
+          const bool mine = j == a.fuse;
+          const float lj = mine ? l0 : lw[ip][j];
+          if (lj == -INFINITY) continue;
+          const float e = __builtin_amdgcn_exp2f((lj - m) * kLog2e);
+          den += e;
+          const f16x8 oj = mine ? own : ow[ip][j];
+          f32x8 of;
+#pragma unroll
+          for (int x = 0; x < 8; ++x) of[x] = static_cast<float>(oj[x]);
+          acc += e * of;
+        }
+        acc *= 1.0f / den;
+        bf16x8 ob;
+#pragma unroll
+        for (int x = 0; x < 8; ++x) ob[x] = (__bf16)acc[x];
+        u16* orow = static_cast<u16*>(a.out) + (((int64_t)it.b * a.N + p) * a.H + it.h) * D + chunk * 8;
+        __builtin_nontemporal_store(ob, reinterpret_cast<bf16x8*>(orow));
+        if (chunk == 0)
+          __builtin_nontemporal_store(m + __builtin_amdgcn_logf(den) * kLn2, a.lse + bh * a.N + p);
+      }
+    }
   }
 }
 
@@ -480,8 +569,33 @@ __global__ __launch_bounds__(kBM32) void attn_fwd_f32(AttnArgs a) {
 
 }  // namespace
 
-hipError_t launch_attention(const Plan& plan, const void* q, const void* k, const void* v,
-                            void* workspace, hipStream_t stream) {
+namespace {
+
+// The plan fuses the combine only for D <= 64.
+template <int D, bool kBuf>
+hipError_t launch_bf16(const dim3& grid, hipStream_t stream, const AttnArgs& a, bool fused) {
+  if (!fused) {
+    hipLaunchKernelGGL((attn_fwd_bf16<D, kBuf, 0>), grid, dim3(kThreads), 0, stream, a);
+  } else if constexpr (D <= 64) {
+    if (a.mix_npat <= 4)
+      hipLaunchKernelGGL((attn_fwd_bf16<D, kBuf, 4>), grid, dim3(kThreads), 0, stream, a);
+    else if (a.mix_npat <= 8)
+      hipLaunchKernelGGL((attn_fwd_bf16<D, kBuf, 8>), grid, dim3(kThreads), 0, stream, a);
+    else
+      hipLaunchKernelGGL((attn_fwd_bf16<D, kBuf, DA_MAX_PATTERNS>), grid, dim3(kThreads), 0, stream, a);
+  } else {
+    return hipErrorInvalidValue;
+  }
+  return hipSuccess;
+}
+
+}  // namespace
+
+hipError_t launch_attention(const Plan& plan, AttnPart part, const void* q, const void* k,
+                            const void* v, void* workspace, void* out, float* lse,
+                            hipStream_t stream) {
+  const bool fused = part == kFusedPattern;
+  if (part != kAllPatterns && (plan.fuse < 0 || plan.dtype != DA_BF16)) return hipErrorInvalidValue;
   AttnArgs a;
   a.q = q;
   a.k = k;
@@ -490,17 +604,27 @@ hipError_t launch_attention(const Plan& plan, const void* q, const void* k, cons
   a.B = static_cast<int32_t>(plan.B);
   a.N = static_cast<int32_t>(plan.N);
   a.H = static_cast<int32_t>(plan.H);
-  a.npat = plan.npat;
   a.causal = plan.causal;
-  a.total_items = static_cast<int32_t>(plan.total_items);
   a.scale_log2 = plan.scale * kLog2e;
+  a.out = out;
+  a.lse = lse;
+  a.mix_npat = plan.npat;
+  a.fuse = plan.fuse;
+  for (int i = 0; i < DA_MAX_PATTERNS; ++i)
+    a.mix[i] = i < plan.npat ? make_mixpat(plan.pat[i]) : MixPat{make_fastdiv(1), make_fastdiv(1), 1, 1, 0, 0};
+  // The patterns of this launch, most query tiles per unit first.
   int order[DA_MAX_PATTERNS];
-  for (int i = 0; i < plan.npat; ++i) order[i] = i;
-  std::stable_sort(order, order + plan.npat,
-                   [&](int x, int y) { return plan.pat[x].ntiles > plan.pat[y].ntiles; });
+  int n = 0;
+  for (int i = 0; i < plan.npat; ++i) {
+    const bool mine = part == kAllPatterns || (part == kFusedPattern) == (i == plan.fuse);
+    if (mine) order[n++] = i;
+  }
+  std::stable_sort(order, order + n, [&](int x, int y) { return plan.pat[x].ntiles > plan.pat[y].ntiles; });
+  a.npat = n;
+  int64_t items = 0, launch = 0;
   for (int i = 0; i < DA_MAX_PATTERNS; ++i) {
     PatArgs& pa = a.pat[i];
-    if (i < plan.npat) {
+    if (i < n) {
       const PatternPlan& pp = plan.pat[order[i]];
       pa.w = static_cast<int32_t>(pp.w);
       pa.r = static_cast<int32_t>(pp.r);
@@ -510,29 +634,34 @@ hipError_t launch_attention(const Plan& plan, const void* q, const void* k, cons
       pa.units = static_cast<int32_t>(pp.units);
       pa.o_off = static_cast<int64_t>(pp.o_off);
       pa.lse_off = static_cast<int64_t>(pp.lse_off);
+      items += pp.units * pp.ntiles;
+      // XCD 0 holds the most units of every pattern; the launch covers 8 times its slots.
+      launch += (pp.units + 7) / 8 * pp.ntiles * 8;
     } else {
       pa = PatArgs{1, 1, 1, 1, 1, 0, 0, 0};
     }
   }
-  if (plan.total_items == 0) return hipSuccess;
-  // XCD 0 holds the most units of every pattern; the launch covers 8 times its slots.
-  const dim3 grid(static_cast<unsigned>(plan.launch_items));
+  a.total_items = static_cast<int32_t>(items);
+  if (items == 0) return hipSuccess;
+  const dim3 grid(static_cast<unsigned>(launch));
   if (plan.dtype == DA_BF16) {
+    hipError_t e;
     switch (plan.D) {
       case 32:
-        if (plan.offsets32) hipLaunchKernelGGL((attn_fwd_bf16<32, true>), grid, dim3(kThreads), 0, stream, a);
-        else hipLaunchKernelGGL((attn_fwd_bf16<32, false>), grid, dim3(kThreads), 0, stream, a);
+        e = plan.offsets32 ? launch_bf16<32, true>(grid, stream, a, fused)
+                           : launch_bf16<32, false>(grid, stream, a, fused);
         break;
       case 64:
-        if (plan.offsets32) hipLaunchKernelGGL((attn_fwd_bf16<64, true>), grid, dim3(kThreads), 0, stream, a);
-        else hipLaunchKernelGGL((attn_fwd_bf16<64, false>), grid, dim3(kThreads), 0, stream, a);
+        e = plan.offsets32 ? launch_bf16<64, true>(grid, stream, a, fused)
+                           : launch_bf16<64, false>(grid, stream, a, fused);
         break;
       case 128:
-        if (plan.offsets32) hipLaunchKernelGGL((attn_fwd_bf16<128, true>), grid, dim3(kThreads), 0, stream, a);
-        else hipLaunchKernelGGL((attn_fwd_bf16<128, false>), grid, dim3(kThreads), 0, stream, a);
+        e = plan.offsets32 ? launch_bf16<128, true>(grid, stream, a, fused)
+                           : launch_bf16<128, false>(grid, stream, a, fused);
         break;
       default: return hipErrorInvalidValue;
     }
+    if (e != hipSuccess) return e;
   } else {
     switch (plan.D) {
       case 32: hipLaunchKernelGGL(attn_fwd_f32<32>, grid, dim3(kBM32), 0, stream, a); break;

@@ -29,21 +29,13 @@ constexpr float kLog2e = 1.442695040888963407f;
 constexpr float kLn2 = 0.693147180559945309f;
 constexpr int kThreads = 256;
 
-struct CombPat {
-  FastDiv fw;       // division by w
-  FastDiv fr;       // division by r
-  int32_t nseg, lmax;
-  int64_t o_off;    // byte offset of the pattern's output rows
-  int64_t lse_off;  // byte offset of the pattern's lse
-};
-
 struct CombArgs {
   const char* ws;
   void* out;
   float* lse;
   int32_t N, H, npat;
   int32_t chunks;  // workgroups per (b, h)
-  CombPat pat[DA_MAX_PATTERNS];
+  MixPat pat[DA_MAX_PATTERNS];
 };
 
 // Eight consecutive workspace elements as loaded (converted to fp32 when used).
@@ -107,7 +99,7 @@ __global__ __launch_bounds__(kThreads) void combine_fwd(CombArgs a) {
     for (int i = 0; i < NP; ++i) {
       li[k][i] = -INFINITY;
       if (i >= a.npat || p >= a.N) continue;
-      const CombPat& P = a.pat[i];
+      const MixPat& P = a.pat[i];
       const uint32_t g = P.fw.div(static_cast<uint32_t>(p));
       const uint32_t pos = static_cast<uint32_t>(p) - g * P.fw.d;
       const uint32_t t = P.fr.div(pos);
@@ -168,18 +160,7 @@ hipError_t launch_combine(const Plan& plan, const void* workspace, void* out, fl
   a.H = static_cast<int32_t>(plan.H);
   a.npat = plan.npat;
   for (int i = 0; i < DA_MAX_PATTERNS; ++i) {
-    CombPat& c = a.pat[i];
-    if (i < plan.npat) {
-      const PatternPlan& pp = plan.pat[i];
-      c.fw = make_fastdiv(static_cast<uint32_t>(pp.w));
-      c.fr = make_fastdiv(static_cast<uint32_t>(pp.r));
-      c.nseg = static_cast<int32_t>(pp.nseg);
-      c.lmax = static_cast<int32_t>(pp.lmax);
-      c.o_off = static_cast<int64_t>(pp.o_off);
-      c.lse_off = static_cast<int64_t>(pp.lse_off);
-    } else {
-      c = CombPat{make_fastdiv(1), make_fastdiv(1), 1, 1, 0, 0};
-    }
+    a.pat[i] = i < plan.npat ? make_mixpat(plan.pat[i]) : MixPat{make_fastdiv(1), make_fastdiv(1), 1, 1, 0, 0};
   }
   const int rows = kThreads / (static_cast<int>(plan.D) / 8) * kRows;  // positions per workgroup
   a.chunks = static_cast<int32_t>((plan.N + rows - 1) / rows);

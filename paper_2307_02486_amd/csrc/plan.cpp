@@ -2,6 +2,7 @@
 #include "plan.h"
 
 #include <cmath>
+#include <cstdlib>
 #include <cstring>
 
 namespace da {
@@ -115,6 +116,17 @@ int make_plan(int64_t B, int64_t N, int64_t H, int64_t D, const da_pattern_t* pa
     if (static_cast<double>(p.pat[i].r) * H * D * esize * 129.0 >= 2147483648.0) p.offsets32 = false;
   // the combine stage launches one workgroup per 8..32 positions of each (b, h)
   if ((N + 7) / 8 * B * H >= (int64_t{1} << 31)) return DA_EINVAL;
+  // Fusing the combine into the attention launch of an r = 1 pattern saves
+  // the separate combine pass; its epilogue's workspace loads are
+  // latency-bound, which pays at D <= 64 (32K tokens, 5 patterns: 0.328 ->
+  // 0.287 ms per call; 256K tokens, 8 patterns: 2.90 -> 2.85 ms) but not at
+  // D = 128, where the kernel runs at occupancy 2 and each item has twice the
+  // row chunks (1M tokens, 6 patterns: 50.2 -> 50.6 ms).
+  p.fuse = -1;
+  const char* sep = std::getenv("DILATED_ATTN_SEPARATE_COMBINE");
+  if (p.dtype == DA_BF16 && D <= 64 && !(sep && sep[0] == '1'))
+    for (int i = 0; i < p.npat && p.fuse < 0; ++i)
+      if (p.pat[i].r == 1) p.fuse = i;
   p.total_items = items;
   p.workspace_bytes = ws;
   p.covered_rows = covered;

@@ -57,6 +57,11 @@ struct Plan {
   int64_t total_items;
   int64_t launch_items;  // workgroups of the attention launch (XCD-balanced, >= total_items)
   bool offsets32;        // every key tile spans < 2^31 bytes: 32-bit buffer offsets suffice
+  // Index of the pattern whose attention launch also runs the combine (the
+  // first pattern with r = 1, which keeps every row), or -1: the combine is
+  // then a separate stage.  Fusing needs bf16 inputs and D <= 64 and is
+  // turned off by setting DILATED_ATTN_SEPARATE_COMBINE=1 in the environment.
+  int fuse;
   uint64_t workspace_bytes;
   int64_t covered_rows;
   double sparse_flops;

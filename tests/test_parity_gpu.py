@@ -174,6 +174,40 @@ def test_scale_argument():
     compare_full(q, k, v, [(64, 1), (200, 2)], True, "bf16", scale=0.3, tag="scale=0.3")
 
 
+FUSE_CASES = [
+    ("n8k_b2_h12_d64_3pat", None),
+    ("n32k_h12_d64_5pat", None),
+    (None, (1, 777, 5, 32, [(256, 1), (512, 7), (1000, 9)], False)),
+    (None, (1, 513, 17, 64, [(512, 1), (513, 20)], True)),
+    (None, (2, 300, 3, 64, [(128, 3), (300, 1), (64, 5), (300, 1)], True)),  # r = 1 not first, twice
+    (None, (1, 1000, 2, 64, [(1000, 1)], True)),                         # the fused pattern alone
+]
+
+
+@pytest.mark.parametrize("wl_name,case", FUSE_CASES, ids=lambda x: str(x)[:40])
+def test_fused_combine_matches_separate(wl_name, case, monkeypatch):
+    """With an r = 1 pattern the combine runs inside that pattern's attention
+    launch; it must give exactly the separate combine kernel's results."""
+    from paper_2307_02486_amd import plan
+    if wl_name is not None:
+        wl = workloads.BY_NAME[wl_name]
+        q, k, v = workloads.make_qkv(wl, device="cuda")
+        pats, causal = list(wl.patterns), wl.causal
+    else:
+        B, N, H, D, pats, causal = case
+        q, k, v = (workloads.make_random((B, N, H, D), torch.bfloat16, 1.0, 400 + N, "cuda", t) for t in range(3))
+    B, N, H, D = q.shape
+    note(f"[fused combine] {wl_name or case}")
+    monkeypatch.delenv("DILATED_ATTN_SEPARATE_COMBINE", raising=False)
+    assert plan(B, N, H, D, pats, causal, torch.bfloat16)["combine_fused"] == 1
+    o1, l1 = run_gpu(q, k, v, pats, causal)
+    monkeypatch.setenv("DILATED_ATTN_SEPARATE_COMBINE", "1")
+    assert plan(B, N, H, D, pats, causal, torch.bfloat16)["combine_fused"] == 0
+    o2, l2 = run_gpu(q, k, v, pats, causal)
+    assert torch.equal(o1, o2), f"out differs: max {float((o1.float() - o2.float()).abs().max())}"
+    assert torch.equal(l1, l2), f"lse differs: max {float((l1 - l2).abs().max())}"
+
+
 def test_deterministic():
     wl = workloads.BY_NAME["n8k_b2_h12_d64_3pat"]
     note("[determinism] n8k")
