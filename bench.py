@@ -341,6 +341,10 @@ def main():
     ms, ms_first, ms_second = timed(args.steps)
     tflops = flops / (ms * 1e-3) / 1e12
     prof = profiled_counters(wl.name)
+    if separate is not None:
+        separate.update({"attention_traffic": prof.get("attention_bytes_per_launch"),
+                         "attention_mfma_busy_pct_profiled": prof.get("separate_attention_mfma_busy_pct"),
+                         "combine_traffic": prof.get("combine_bytes_per_launch")})
     if fused:
         # Both launches run the attention kernel; the second also mixes the patterns.
         ms_attn = ms_first + ms_second
