@@ -78,7 +78,7 @@ struct SmemBf16 {
 // kMixNP = 0: the per-pattern rows go to the workspace.  kMixNP > 0: this
 // launch computes a pattern with r = 1 after every other pattern's rows are
 // in the workspace, and its epilogue mixes them (kMixNP >= the call's pattern
-// count bounds the mixing loops at compile time).
+// count bounds the mixing loops at compile time: 4, 5, 8 or 16).
 template <int D, bool kBufferLoads, int kMixNP>
 __global__ __launch_bounds__(kThreads) void attn_fwd_bf16(AttnArgs a) {
   static_assert(D % 32 == 0, "head dim must be a multiple of 32");
@@ -408,7 +408,10 @@ __global__ __launch_bounds__(kThreads) void attn_fwd_bf16(AttnArgs a) {
     float* lse_stg = reinterpret_cast<float*>(&sm.v[0][0]) + wv * 32;
     if (hi == 0) lse_stg[qr] = lse_own;
     constexpr int NP = kMixNP;
-    constexpr int PG = NP >= 16 ? 1 : 16 / NP;  // passes whose loads are in flight together
+    // Passes whose loads are in flight together: all of them for up to 5
+    // patterns (one round of memory latency), else as many as 16 pattern
+    // slots allow (more would cost occupancy).
+    constexpr int PG = NP >= 16 ? 1 : (NP <= 5 ? kPasses : 16 / NP);
     const int64_t bh = (int64_t)it.b * a.H + it.h;
 #pragma unroll
     for (int i0 = 0; i0 < kPasses; i0 += PG) {
@@ -579,6 +582,8 @@ hipError_t launch_bf16(const dim3& grid, hipStream_t stream, const AttnArgs& a, 
   } else if constexpr (D <= 64) {
     if (a.mix_npat <= 4)
       hipLaunchKernelGGL((attn_fwd_bf16<D, kBuf, 4>), grid, dim3(kThreads), 0, stream, a);
+    else if (a.mix_npat <= 5)
+      hipLaunchKernelGGL((attn_fwd_bf16<D, kBuf, 5>), grid, dim3(kThreads), 0, stream, a);
     else if (a.mix_npat <= 8)
       hipLaunchKernelGGL((attn_fwd_bf16<D, kBuf, 8>), grid, dim3(kThreads), 0, stream, a);
     else

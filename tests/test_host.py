@@ -80,22 +80,27 @@ def test_plan_accounting_matches_enumeration(wl):
     assert info["bytes_combine"] == rows * (wl.D * ws + 4) + wl.B * wl.N * wl.H * (wl.D * es + 4)
 
 
-@pytest.mark.parametrize("D,dtype,pats,env,fused", [
-    (64, torch.bfloat16, [(2048, 1), (4096, 2)], None, 1),
-    (32, torch.bfloat16, [(64, 3), (128, 1)], None, 1),    # the r = 1 pattern need not come first
-    (64, torch.bfloat16, [(64, 3), (128, 2)], None, 0),    # no pattern keeps every row
-    (128, torch.bfloat16, [(2048, 1), (4096, 2)], None, 0),  # D = 128: separate combine
-    (64, torch.float32, [(2048, 1)], None, 0),             # fp32: separate combine
-    (64, torch.bfloat16, [(2048, 1), (4096, 2)], "1", 0),  # turned off by the environment
-    (64, torch.bfloat16, [(2048, 1), (4096, 2)], "0", 1),
+BENCH_PATS = [(2048, 1), (4096, 2), (8192, 4), (16384, 6), (32768, 12)]
+
+
+@pytest.mark.parametrize("N,H,D,dtype,pats,env,fused", [
+    (32768, 12, 64, torch.bfloat16, BENCH_PATS, None, 1),   # 3096 items besides (2048, 1)
+    (32768, 12, 32, torch.bfloat16, BENCH_PATS[::-1], None, 1),  # the r = 1 pattern need not come first
+    (8192, 12, 64, torch.bfloat16, BENCH_PATS[:3], None, 0),     # 576 items besides: too few
+    (8192, 12, 64, torch.bfloat16, BENCH_PATS[:3], "0", 1),      # ... unless forced
+    (32768, 12, 64, torch.bfloat16, [(64, 3), (128, 2)], "0", 0),  # no pattern keeps every row
+    (32768, 12, 128, torch.bfloat16, BENCH_PATS, None, 0),  # D = 128: separate combine
+    (32768, 12, 128, torch.bfloat16, BENCH_PATS, "0", 0),
+    (32768, 12, 64, torch.float32, BENCH_PATS, "0", 0),     # fp32: separate combine
+    (32768, 12, 64, torch.bfloat16, BENCH_PATS, "1", 0),    # turned off by the environment
 ])
-def test_plan_combine_fused(D, dtype, pats, env, fused, monkeypatch):
+def test_plan_combine_fused(N, H, D, dtype, pats, env, fused, monkeypatch):
     from paper_2307_02486_amd import plan
     if env is None:
         monkeypatch.delenv("DILATED_ATTN_SEPARATE_COMBINE", raising=False)
     else:
         monkeypatch.setenv("DILATED_ATTN_SEPARATE_COMBINE", env)
-    assert plan(1, 4096, 4, D, pats, True, dtype)["combine_fused"] == fused
+    assert plan(1, N, H, D, pats, True, dtype)["combine_fused"] == fused
 
 
 def test_plan_accounting_random_small():
