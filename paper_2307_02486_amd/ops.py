@@ -90,8 +90,12 @@ def dilated_attn(q: torch.Tensor, k: torch.Tensor, v: torch.Tensor,
 
 
 class StageTimer:
-    """Context manager around dilated_attn_profile_begin/end: per-stage HIP
-    event timing of the calls made inside it (on each call's own stream)."""
+    """Context manager around dilated_attn_profile_begin/end: HIP event timing
+    of the two launches of each call made inside it (on the call's own
+    stream).  ms_attention and ms_combine sum the first and second launch:
+    the attention and the combine stage, or, with the combine fused
+    (plan(...)["combine_fused"]), the attention launch of the patterns other
+    than the fused one and the fused pattern's launch with the combine."""
 
     def __init__(self, capacity: int = 4096):
         self.capacity = capacity
