@@ -2,20 +2,21 @@
 
 One step = one dilated_attn_fwd call over the N=32768, H=12, D=64 bf16
 workload with the five patterns (2048,1) (4096,2) (8192,4) (16384,6)
-(32768,12), inputs resident in HBM.  With bf16 inputs and an r = 1 pattern the
-call is two launches of the attention kernel: every other pattern, then the
-r = 1 pattern with the combine fused into its epilogue.
+(32768,12), inputs resident in HBM.  The call is two launches: the attention
+kernel over every pattern, then the kernel that mixes the patterns.
 
 Prints one JSON line: effective TFLOP/s over the exact sparse flops (4*D per
 unmasked query-key pair) and tokens/s of the timed back-to-back steps, the
 times of the call's two launches from a second pass in which the library
 records HIP events around them on the call's stream, the attention kernel's
-MFMA roofline fraction, the same figures for the path with a separate combine
-kernel (DILATED_ATTN_SEPARATE_COMBINE=1) including that kernel's HBM
-bandwidth, and the CPU oracle timed on a bounded sample on this host.  After
-the timed region, a further pass times each step on its own (median, minimum,
-mean), once as is and once with a 512 MiB buffer written before each step so
-that the inputs are no longer held in the Infinity Cache.
+MFMA roofline fraction and the combine kernel's HBM bandwidth, the same
+figures for the opt-in path that fuses the combine into the epilogue of the
+r = 1 pattern's attention launch (DILATED_ATTN_FUSE_COMBINE=1), and the CPU
+oracle timed on a bounded sample on this host.  Every timed region follows at
+least --warmup-seconds of untimed calls.  After the timed region, a further
+pass times each step on its own (median, minimum, mean), once as is and once
+with a 512 MiB buffer written before each step so that the inputs are no
+longer held in the Infinity Cache.
 """
 from __future__ import annotations
 
@@ -41,6 +42,9 @@ def parse():
     ap.add_argument("--gpus", type=int, default=1)
     ap.add_argument("--steps", type=int, default=50)
     ap.add_argument("--warmup", type=int, default=5)
+    ap.add_argument("--warmup-seconds", type=float, default=1.0,
+                    help="untimed calls continue until at least this long has passed (the GPU raises "
+                         "its clocks only after some time under load)")
     ap.add_argument("--workload", default=DEFAULT_WORKLOAD)
     ap.add_argument("--cpu-seconds", type=float, default=12.0,
                     help="minimum CPU time spent on the oracle sample (0 skips the CPU baseline)")
@@ -185,8 +189,11 @@ def sweep(args):
             out = torch.empty_like(q)
             lse = torch.empty((wl.B, wl.H, wl.N), dtype=torch.float32, device=dev)
             ws = workspace_for(q, pats, wl.causal)
-            for _ in range(warm):
+            t0, n = time.perf_counter(), 0
+            while n < warm or time.perf_counter() - t0 < min(args.warmup_seconds, 0.5):
                 dilated_attn(q, k, v, pats, wl.causal, out=out, lse=lse, workspace=ws, stream=stream)
+                torch.cuda.synchronize()
+                n += 1
             times = []
             for _ in range(steps):
                 e0 = torch.cuda.Event(enable_timing=True)
@@ -232,9 +239,11 @@ def backward(args):
     def step():
         dilated_attn_bwd(q, k, v, out, lse, dout, pats, wl.causal, dq=dq, dk=dk, dv=dv, workspace=ws, stream=stream)
 
-    for _ in range(args.warmup):
+    t0, n = time.perf_counter(), 0
+    while n < args.warmup or time.perf_counter() - t0 < args.warmup_seconds:
         step()
-    torch.cuda.synchronize()
+        n += 1
+        torch.cuda.synchronize()
     e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
     e0.record(stream)
     for _ in range(args.steps):
@@ -298,12 +307,22 @@ def main():
     def step():
         dilated_attn(q, k, v, pats, wl.causal, out=out, lse=lse, workspace=ws, stream=stream)
 
+    def warm():
+        """At least `warmup` untimed calls, and calls for at least
+        `warmup_seconds`: a short warm-up leaves the GPU at a lower clock and
+        the first timed region up to 10 % slower than later ones."""
+        t0 = time.perf_counter()
+        n = 0
+        while n < args.warmup or time.perf_counter() - t0 < args.warmup_seconds:
+            for _ in range(5):
+                step()
+            n += 5
+            torch.cuda.synchronize()
+
     def timed(steps):
         """Mean ms per call over `steps` back-to-back calls, then the mean ms
         of the call's two launches over as many calls again."""
-        for _ in range(args.warmup):
-            step()
-        torch.cuda.synchronize()
+        warm()
         t_start = torch.cuda.Event(enable_timing=True)
         t_end = torch.cuda.Event(enable_timing=True)
         # Timed region: exactly `steps` back-to-back calls, nothing else on the stream.
@@ -323,37 +342,40 @@ def main():
     flops = info["sparse_flops"]
     peak = PEAK_BF16_TFLOPS if wl.dtype == "bf16" else PEAK_F32_TFLOPS
     fused = bool(info["combine_fused"])
-    separate = None
-    if fused:
-        # The path with a separate combine kernel, for that kernel's bandwidth.
-        os.environ["DILATED_ATTN_SEPARATE_COMBINE"] = "1"
-        try:
-            s_ms, s_attn, s_comb = timed(args.steps)
-        finally:
-            del os.environ["DILATED_ATTN_SEPARATE_COMBINE"]
-        s_gbs = info["bytes_combine"] / (s_comb * 1e-3) / 1e9
-        s_tf = flops / (s_attn * 1e-3) / 1e12
-        separate = {"ms_per_step": round(s_ms, 5), "tflops": round(flops / (s_ms * 1e-3) / 1e12, 3),
-                    "attention_ms": round(s_attn, 5), "attention_tflops": round(s_tf, 3),
-                    "attention_frac_of_mfma_peak": round(s_tf / peak, 4),
-                    "combine_ms": round(s_comb, 5), "combine_algorithmic_bytes": info["bytes_combine"],
-                    "combine_gbps": round(s_gbs, 1), "combine_frac_of_hbm_peak": round(s_gbs / PEAK_HBM_GBS, 4)}
     ms, ms_first, ms_second = timed(args.steps)
-    tflops = flops / (ms * 1e-3) / 1e12
     prof = profiled_counters(wl.name)
-    if separate is not None:
-        separate.update({"attention_traffic": prof.get("attention_bytes_per_launch"),
-                         "attention_mfma_busy_pct_profiled": prof.get("separate_attention_mfma_busy_pct"),
-                         "combine_traffic": prof.get("combine_bytes_per_launch")})
+
+    fused_path = None
+    if not fused and os.environ.get("DILATED_ATTN_FUSE_COMBINE") is None:
+        # The opt-in path with the combine in the r = 1 pattern's attention launch.
+        os.environ["DILATED_ATTN_FUSE_COMBINE"] = "1"
+        try:
+            if plan(wl.B, wl.N, wl.H, wl.D, pats, wl.causal, wl.torch_dtype)["combine_fused"]:
+                f_ms, f_first, f_second = timed(args.steps)
+                f_tf = flops / ((f_first + f_second) * 1e-3) / 1e12
+                fused_path = {
+                    "ms_per_step": round(f_ms, 5), "tflops": round(flops / (f_ms * 1e-3) / 1e12, 3),
+                    "launch_other_patterns_ms": round(f_first, 5),
+                    "launch_fused_pattern_with_combine_ms": round(f_second, 5),
+                    "attention_with_combine_tflops": round(f_tf, 3),
+                    "attention_with_combine_frac_of_mfma_peak": round(f_tf / peak, 4),
+                    "traffic": prof.get("fused_attention_bytes_per_call"),
+                    "mfma_busy_pct_profiled": prof.get("fused_attention_mfma_busy_pct")}
+        finally:
+            del os.environ["DILATED_ATTN_FUSE_COMBINE"]
+
+    tflops = flops / (ms * 1e-3) / 1e12
     if fused:
         # Both launches run the attention kernel; the second also mixes the patterns.
         ms_attn = ms_first + ms_second
         traffic = prof.get("fused_attention_bytes_per_call")
+        busy = prof.get("fused_attention_mfma_busy_pct")
         stages = {"launch_other_patterns_ms": round(ms_first, 5),
                   "launch_fused_pattern_with_combine_ms": round(ms_second, 5)}
     else:
         ms_attn = ms_first
         traffic = prof.get("attention_bytes_per_launch")
+        busy = prof.get("attention_mfma_busy_pct")
         stages = {"attention_ms": round(ms_first, 5), "combine_ms": round(ms_second, 5)}
     attn_tflops = flops / (ms_attn * 1e-3) / 1e12
     comb_gbs = info["bytes_combine"] / (ms_second * 1e-3) / 1e9
@@ -377,17 +399,18 @@ def main():
         "launches": stages,
         "attention_stage": {"ms": round(ms_attn, 5), "tflops": round(attn_tflops, 3),
                             "frac_of_mfma_peak": round(attn_tflops / peak, 4),
-                            "mfma_busy_pct_profiled": prof.get("attention_mfma_busy_pct")},
+                            "mfma_busy_pct_profiled": busy},
         "combine_stage": ({"fused_into_attention": True} if fused else
                           {"ms": round(ms_second, 5), "algorithmic_bytes": info["bytes_combine"],
                            "gbps": round(comb_gbs, 1), "frac_of_hbm_peak": round(comb_gbs / PEAK_HBM_GBS, 4),
                            "traffic": prof.get("combine_bytes_per_launch")}),
-        "separate_combine_path": separate,
+        "fused_combine_path": fused_path,
         "roofline": {"bound": "mfma", "achieved": round(attn_tflops, 3), "peak": peak,
                      "unit": "TFLOP/s", "frac": round(attn_tflops / peak, 4), "traffic": traffic},
         "cpu_baseline": None,
     }
     if args.dist_steps > 0:
+        warm()
         res["step_distribution"] = {
             "unflushed": step_distribution(step, stream, args.dist_steps, 0),
             "flushed_512MiB": step_distribution(step, stream, args.dist_steps, 512 << 20),

@@ -79,12 +79,10 @@ typedef struct {
   int64_t combine_fused;    /* 1: fwd runs the combine inside the attention
                                kernel of the first pattern with r = 1, as a
                                second attention launch after the other
-                               patterns' (bf16 inputs, D <= 64, at least 2048
-                               work items in the other patterns; the
-                               environment variable
-                               DILATED_ATTN_SEPARATE_COMBINE = "1" turns this
-                               off, "0" drops the work-item condition);
-                               0: a separate combine kernel                   */
+                               patterns'; opt-in, with the environment
+                               variable DILATED_ATTN_FUSE_COMBINE = "1", for
+                               bf16 inputs and D <= 64.  0: a separate
+                               combine kernel (the default)                  */
 } da_plan_info_t;
 
 /*

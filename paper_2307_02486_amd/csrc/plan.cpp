@@ -26,10 +26,6 @@ int block_m_for(int dtype) { return dtype == DA_BF16 ? 32 * DA_BF16_WAVES : 64; 
 namespace {
 
 constexpr uint64_t kAlign = 256;
-// Work items the other patterns' launch needs before the combine is fused:
-// about 2.7 rounds of the attention kernel's 768 workgroup slots at D = 64
-// (256 CUs x 3).
-constexpr int64_t kFuseMinItems = 2048;
 
 uint64_t align_up(uint64_t x) { return (x + kAlign - 1) / kAlign * kAlign; }
 
@@ -120,29 +116,18 @@ int make_plan(int64_t B, int64_t N, int64_t H, int64_t D, const da_pattern_t* pa
     if (static_cast<double>(p.pat[i].r) * H * D * esize * 129.0 >= 2147483648.0) p.offsets32 = false;
   // the combine stage launches one workgroup per 8..32 positions of each (b, h)
   if ((N + 7) / 8 * B * H >= (int64_t{1} << 31)) return DA_EINVAL;
-  // Fusing the combine into the attention launch of an r = 1 pattern saves
-  // the separate combine pass but splits the attention work into two
-  // launches.  Measured: it pays at D <= 64 when the first launch (the other
-  // patterns) has enough work items to fill the GPU several times over (32K
-  // tokens, 5 patterns, 3096 items: 0.324 -> 0.284 ms per call; 256K tokens,
-  // 8 patterns: 2.90 -> 2.85 ms), not when that launch is short (8K tokens,
-  // B = 2, 3 patterns, 1152 items: 0.136 -> 0.144 ms), nor at D = 128, where
-  // the kernel runs at occupancy 2 and the epilogue's latency-bound loads
-  // cover twice the row chunks (1M tokens, 6 patterns: 50.2 -> 50.6 ms).
-  // DILATED_ATTN_SEPARATE_COMBINE=1 turns fusing off, =0 fuses whenever
-  // possible (bf16, D <= 64, an r = 1 pattern) regardless of the work size.
+  // The combine can run inside the attention launch of an r = 1 pattern
+  // (see Plan::fuse).  Measured with a warmed-up GPU, calls alternating
+  // between the two paths in one process: within 1 % of the separate combine
+  // at 32K and 256K tokens (D = 64) although it moves 19 % fewer HBM bytes,
+  // 6 % slower at 8K tokens (B = 2) and 0.1 % at D = 128 (1M tokens).  It is
+  // therefore opt-in: DILATED_ATTN_FUSE_COMBINE=1 in the environment fuses
+  // whenever the call allows it (bf16, D <= 64, a pattern with r = 1).
   p.fuse = -1;
-  const char* sep = std::getenv("DILATED_ATTN_SEPARATE_COMBINE");
-  const bool force = sep && sep[0] == '0';
-  if (p.dtype == DA_BF16 && D <= 64 && !(sep && sep[0] == '1')) {
-    int cand = -1;
-    for (int i = 0; i < p.npat && cand < 0; ++i)
-      if (p.pat[i].r == 1) cand = i;
-    int64_t other_items = 0;
-    for (int i = 0; i < p.npat; ++i)
-      if (i != cand) other_items += p.pat[i].units * p.pat[i].ntiles;
-    if (cand >= 0 && (force || other_items >= kFuseMinItems)) p.fuse = cand;
-  }
+  const char* fz = std::getenv("DILATED_ATTN_FUSE_COMBINE");
+  if (fz && fz[0] == '1' && p.dtype == DA_BF16 && D <= 64)
+    for (int i = 0; i < p.npat && p.fuse < 0; ++i)
+      if (p.pat[i].r == 1) p.fuse = i;
   p.total_items = items;
   p.workspace_bytes = ws;
   p.covered_rows = covered;

@@ -59,9 +59,8 @@ struct Plan {
   bool offsets32;        // every key tile spans < 2^31 bytes: 32-bit buffer offsets suffice
   // Index of the pattern whose attention launch also runs the combine (the
   // first pattern with r = 1, which keeps every row), or -1: the combine is
-  // then a separate stage.  Fusing needs bf16 inputs, D <= 64 and at least
-  // 2048 work items in the other patterns; DILATED_ATTN_SEPARATE_COMBINE=1 in
-  // the environment turns it off, =0 drops the work-size condition.
+  // a separate stage.  Fusing is opt-in (DILATED_ATTN_FUSE_COMBINE=1 in the
+  // environment) and needs bf16 inputs and D <= 64.
   int fuse;
   uint64_t workspace_bytes;
   int64_t covered_rows;

@@ -84,22 +84,20 @@ BENCH_PATS = [(2048, 1), (4096, 2), (8192, 4), (16384, 6), (32768, 12)]
 
 
 @pytest.mark.parametrize("N,H,D,dtype,pats,env,fused", [
-    (32768, 12, 64, torch.bfloat16, BENCH_PATS, None, 1),   # 3096 items besides (2048, 1)
-    (32768, 12, 32, torch.bfloat16, BENCH_PATS[::-1], None, 1),  # the r = 1 pattern need not come first
-    (8192, 12, 64, torch.bfloat16, BENCH_PATS[:3], None, 0),     # 576 items besides: too few
-    (8192, 12, 64, torch.bfloat16, BENCH_PATS[:3], "0", 1),      # ... unless forced
-    (32768, 12, 64, torch.bfloat16, [(64, 3), (128, 2)], "0", 0),  # no pattern keeps every row
-    (32768, 12, 128, torch.bfloat16, BENCH_PATS, None, 0),  # D = 128: separate combine
-    (32768, 12, 128, torch.bfloat16, BENCH_PATS, "0", 0),
-    (32768, 12, 64, torch.float32, BENCH_PATS, "0", 0),     # fp32: separate combine
-    (32768, 12, 64, torch.bfloat16, BENCH_PATS, "1", 0),    # turned off by the environment
+    (32768, 12, 64, torch.bfloat16, BENCH_PATS, None, 0),       # separate combine by default
+    (32768, 12, 64, torch.bfloat16, BENCH_PATS, "1", 1),        # opt-in
+    (8192, 12, 32, torch.bfloat16, BENCH_PATS[::-1], "1", 1),   # the r = 1 pattern need not come first
+    (32768, 12, 64, torch.bfloat16, [(64, 3), (128, 2)], "1", 0),  # no pattern keeps every row
+    (32768, 12, 128, torch.bfloat16, BENCH_PATS, "1", 0),       # D = 128: separate combine
+    (32768, 12, 64, torch.float32, BENCH_PATS, "1", 0),         # fp32: separate combine
+    (32768, 12, 64, torch.bfloat16, BENCH_PATS, "0", 0),
 ])
 def test_plan_combine_fused(N, H, D, dtype, pats, env, fused, monkeypatch):
     from paper_2307_02486_amd import plan
     if env is None:
-        monkeypatch.delenv("DILATED_ATTN_SEPARATE_COMBINE", raising=False)
+        monkeypatch.delenv("DILATED_ATTN_FUSE_COMBINE", raising=False)
     else:
-        monkeypatch.setenv("DILATED_ATTN_SEPARATE_COMBINE", env)
+        monkeypatch.setenv("DILATED_ATTN_FUSE_COMBINE", env)
     assert plan(1, N, H, D, pats, True, dtype)["combine_fused"] == fused
 
 
