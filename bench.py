@@ -62,14 +62,31 @@ def parse():
 
 
 def copy_calibration(mib):
-    """A plain copy of a known number of bytes (read mib MiB, write mib MiB)."""
+    """A plain copy of a known number of bytes (read mib MiB, write mib MiB),
+    five launches for the counters, then the same copy timed back to back
+    after a warm-up (bytes read plus bytes written per second): the HBM rate
+    a streaming kernel of that size reaches in practice."""
     import torch
     x = torch.ones(mib * (1 << 20) // 4, dtype=torch.float32, device="cuda")
     y = torch.empty_like(x)
     for _ in range(5):
         y.copy_(x)
     torch.cuda.synchronize()
-    print(json.dumps({"copy_calibration_bytes_each_way": mib * (1 << 20), "launches": 5}), flush=True)
+    t0 = time.perf_counter()
+    while time.perf_counter() - t0 < 1.0:
+        y.copy_(x)
+        torch.cuda.synchronize()
+    reps = max(5, int(2e10 // (mib << 20)))
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    e0.record()
+    for _ in range(reps):
+        y.copy_(x)
+    e1.record()
+    torch.cuda.synchronize()
+    ms = e0.elapsed_time(e1) / reps
+    print(json.dumps({"copy_calibration_bytes_each_way": mib * (1 << 20), "launches": 5, "timed_copies": reps,
+                      "ms_per_copy": round(ms, 5), "gbps_read_plus_write": round(2 * (mib << 20) / (ms * 1e-3) / 1e9, 1)}),
+          flush=True)
 
 
 def profiled_counters(workload):

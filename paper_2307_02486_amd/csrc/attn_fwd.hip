@@ -435,9 +435,10 @@ __global__ __launch_bounds__(kThreads) void attn_fwd_bf16(AttnArgs a) {
           const uint32_t sj = static_cast<uint32_t>(it.h) - M.fr.div(static_cast<uint32_t>(it.h)) * M.fr.d;
           if (pos - t * M.fr.d != sj) continue;
           const int64_t wrow = (bh * M.nseg + g) * M.lmax + t;
-          lw[ip][j] = __builtin_nontemporal_load(reinterpret_cast<const float*>(a.ws + M.lse_off) + wrow);
-          ow[ip][j] = __builtin_nontemporal_load(
-              reinterpret_cast<const f16x8*>(reinterpret_cast<const _Float16*>(a.ws + M.o_off) + wrow * D + chunk * 8));
+          // plain loads: the previous launch just wrote these rows, and part
+          // of them is still held in the L2 and the Infinity Cache
+          lw[ip][j] = reinterpret_cast<const float*>(a.ws + M.lse_off)[wrow];
+          ow[ip][j] = *reinterpret_cast<const f16x8*>(reinterpret_cast<const _Float16*>(a.ws + M.o_off) + wrow * D + chunk * 8);
         }
       }
 #pragma unroll

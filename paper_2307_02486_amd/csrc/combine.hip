@@ -43,11 +43,14 @@ template <typename WsT> struct Vec8;
 template <> struct Vec8<_Float16> { typedef f16x8 type; };
 template <> struct Vec8<float> { typedef f32x8 type; };
 
-// Workspace rows and lse values are read exactly once: nontemporal loads.
+// Workspace rows and lse values are read exactly once, but the attention
+// launch just wrote them and part of them is still held in the L2 and the
+// Infinity Cache: plain loads, which can hit there (nontemporal loads
+// measured 9 % slower on the 32K-token workload, equal at 256K).
 template <typename WsT>
 __device__ inline typename Vec8<WsT>::type load8(const WsT* p) {
   typedef typename Vec8<WsT>::type V;
-  return __builtin_nontemporal_load(reinterpret_cast<const V*>(p));
+  return *reinterpret_cast<const V*>(p);
 }
 
 __device__ inline f32x8 to_f32(const f16x8& h) {
@@ -106,7 +109,7 @@ __global__ __launch_bounds__(kThreads) void combine_fwd(CombArgs a) {
       const uint32_t s = static_cast<uint32_t>(h) - P.fr.div(static_cast<uint32_t>(h)) * P.fr.d;
       if (pos - t * P.fr.d != s) continue;
       const int64_t row = ((int64_t)bh * P.nseg + g) * P.lmax + t;
-      li[k][i] = __builtin_nontemporal_load(reinterpret_cast<const float*>(a.ws + P.lse_off) + row);
+      li[k][i] = reinterpret_cast<const float*>(a.ws + P.lse_off)[row];
       o[k][i] = load8(reinterpret_cast<const WsT*>(a.ws + P.o_off) + row * D + d0);
     }
   }
