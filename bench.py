@@ -91,10 +91,10 @@ def copy_calibration(mib):
 
 def profiled_counters(workload):
     """Per-launch figures measured with rocprofv3 counters for the current
-    attention source: HBM bytes of the attention and combine kernels
+    kernel sources: HBM bytes of the attention and combine kernels
     (FETCH_SIZE / WRITE_SIZE scaled by a plain copy of known size) and the
-    attention kernel's MFMA busy percentage.  Empty when the attention kernel's
-    source changed since the measurement."""
+    attention kernel's MFMA busy percentage.  Empty when the attention or the
+    combine kernel's source changed since the measurement."""
     import hashlib
     if not os.path.exists(PROFILED_TRAFFIC):
         return {}
@@ -102,11 +102,12 @@ def profiled_counters(workload):
         rec = json.load(f).get(workload)
     if not rec:
         return {}
-    src = os.path.join(ROOT, "paper_2307_02486_amd", "csrc", "attn_fwd.hip")
-    with open(src, "rb") as f:
-        sha = hashlib.sha256(f.read()).hexdigest()[:16]
-    if sha != rec.get("attn_fwd_hip_sha256_16"):
-        return {}
+    for name in ("attn_fwd", "combine"):
+        src = os.path.join(ROOT, "paper_2307_02486_amd", "csrc", name + ".hip")
+        with open(src, "rb") as f:
+            sha = hashlib.sha256(f.read()).hexdigest()[:16]
+        if sha != rec.get(name + "_hip_sha256_16"):
+            return {}
     return rec
 
 
