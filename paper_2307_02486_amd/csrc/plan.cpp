@@ -118,11 +118,11 @@ int make_plan(int64_t B, int64_t N, int64_t H, int64_t D, const da_pattern_t* pa
   if ((N + 7) / 8 * B * H >= (int64_t{1} << 31)) return DA_EINVAL;
   // The combine can run inside the attention launch of an r = 1 pattern
   // (see Plan::fuse).  Measured with a warmed-up GPU, calls alternating
-  // between the two paths in one process: within 1 % of the separate combine
-  // at 32K and 256K tokens (D = 64) although it moves 19 % fewer HBM bytes,
-  // 6 % slower at 8K tokens (B = 2) and 0.1 % at D = 128 (1M tokens).  It is
-  // therefore opt-in: DILATED_ATTN_FUSE_COMBINE=1 in the environment fuses
-  // whenever the call allows it (bf16, D <= 64, a pattern with r = 1).
+  // between the two paths in one process: 1 % slower than the separate
+  // combine at 32K tokens and equal at 256K (D = 64) although it moves 19 %
+  // fewer HBM bytes, 8 % slower at 8K tokens (B = 2).  It is therefore
+  // opt-in: DILATED_ATTN_FUSE_COMBINE=1 in the environment fuses whenever the
+  // call allows it (bf16, D <= 64, a pattern with r = 1).
   p.fuse = -1;
   const char* fz = std::getenv("DILATED_ATTN_FUSE_COMBINE");
   if (fz && fz[0] == '1' && p.dtype == DA_BF16 && D <= 64)
