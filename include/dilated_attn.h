@@ -184,6 +184,40 @@ int dilated_attn_bwd(const void* q, const void* k, const void* v, const void* ou
                      int64_t causal, int64_t dtype, float softmax_scale,
                      void* workspace, uint64_t workspace_bytes, void* stream);
 
+/*
+ * dilated_attn_xpos - the xPos relative position encoding (Sun et al.,
+ * "A Length-Extrapolatable Transformer", 2022), which the paper's language
+ * model applies to queries and keys before its dilated attention (Sec. 4.1).
+ *
+ * For the row at sequence position n (0-based) of each (b, h) and each pair
+ * of head-dimension elements (2i, 2i+1), i < D/2:
+ *   y[2i]   = s * (x[2i] * cos(a) - x[2i+1] * sin(a))
+ *   y[2i+1] = s * (x[2i] * sin(a) + x[2i+1] * cos(a))
+ * with a = n * base^(-2i/D), s = zeta_i^(sign * (n - center) / scale_base)
+ * and zeta_i = (2i/D + gamma) / (1 + gamma).  sign = +1 for queries and -1
+ * for keys: a query at n and a key at m then meet with factors that depend
+ * on n - m only (center cancels; it keeps the separate factors in range).
+ * transpose = 1 applies the transpose instead (angle -a, the same s), the map
+ * a backward pass multiplies the incoming gradient by.
+ *
+ * x, y        device pointers, [B, N, H, D] of dtype, 16-byte aligned; y may
+ *             equal x (in place) but must not overlap it otherwise.
+ * D           a multiple of 8, 8 <= D <= 256.
+ * center      in [0, N).
+ * base > 1, gamma > 0, scale_base > 0, all finite.  The scale exponents
+ *             |n - center| / scale_base * |log2 zeta_i| must stay <= 64 for
+ *             every position and pair (so that no factor leaves a 2^+-64
+ *             range), else DA_EINVAL: with gamma = 0.4 and scale_base = 512
+ *             about 36K positions around the center.
+ * stream      a hipStream_t (NULL = the default stream); asynchronous.
+ *
+ * Arithmetic in float32, the angle formed and reduced in float64; y rounded
+ * to dtype.  Returns DA_OK or a negative code; errors launch nothing.
+ */
+int dilated_attn_xpos(const void* x, void* y, int64_t B, int64_t N, int64_t H, int64_t D,
+                      int64_t sign, int64_t transpose, int64_t center, float base, float gamma,
+                      float scale_base, int64_t dtype, void* stream);
+
 /* Human-readable text for an error code (static storage, never NULL). */
 const char* dilated_attn_strerror(int code);
 

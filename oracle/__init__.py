@@ -1,4 +1,5 @@
-"""CPU oracle for LongNet dilated attention (forward and backward).  TEST INFRASTRUCTURE ONLY.
+"""CPU oracle for LongNet dilated attention (forward and backward) and, in
+layer_ref, the LongNet attention layer around it.  TEST INFRASTRUCTURE ONLY.
 
 Only the tests, the smoke check and the benchmark's CPU-baseline leg may import
 this package.  The product path (the HIP library and its Python binding) never

@@ -1,6 +1,8 @@
 // C ABI of the dilated-attention forward and backward passes (declared in include/dilated_attn.h).
 #include <hip/hip_runtime.h>
 
+#include <algorithm>
+#include <cmath>
 #include <cstdint>
 #include <vector>
 
@@ -161,6 +163,34 @@ int dilated_attn_bwd(const void* q, const void* k, const void* v, const void* ou
 
   hipStream_t s = static_cast<hipStream_t>(stream);
   if (da::launch_backward(p, l, q, k, v, out, lse, dout, dq, dk, dv, workspace, s) != hipSuccess)
+    return DA_EHIP;
+  return DA_OK;
+}
+
+int dilated_attn_xpos(const void* x, void* y, int64_t B, int64_t N, int64_t H, int64_t D,
+                      int64_t sign, int64_t transpose, int64_t center, float base, float gamma,
+                      float scale_base, int64_t dtype, void* stream) {
+  if (!x || !y) return DA_EINVAL;
+  if (B <= 0 || N <= 0 || H <= 0 || D < 8 || D > 256 || D % 8 != 0) return DA_EINVAL;
+  if (dtype != DA_BF16 && dtype != DA_F32) return DA_EUNSUPPORTED;
+  if ((sign != 1 && sign != -1) || (transpose != 0 && transpose != 1)) return DA_EINVAL;
+  if (center < 0 || center >= N) return DA_EINVAL;
+  if (!std::isfinite(base) || !(base > 1.0f) || !std::isfinite(gamma) || !(gamma > 0.0f) ||
+      !std::isfinite(scale_base) || !(scale_base > 0.0f))
+    return DA_EINVAL;
+  if (B > (int64_t{1} << 40) / N || B * N > (int64_t{1} << 40) / H ||
+      B * N * H > (int64_t{1} << 40) / D)
+    return DA_EINVAL;
+  // zeta_i ranges over [gamma / (1 + gamma), 1): the smallest gives the
+  // largest |log2 zeta| (every zeta_i < 1 for gamma > 0 and i < D/2).
+  const double l2z = std::fabs(std::log2(static_cast<double>(gamma) / (1.0 + gamma)));
+  const double far = static_cast<double>(std::max(center, N - 1 - center));
+  if (far / scale_base * l2z > 64.0) return DA_EINVAL;
+  if (!aligned16(x) || !aligned16(y)) return DA_EALIGN;
+  const uint64_t bytes = static_cast<uint64_t>(B * N * H * D) * (dtype == DA_BF16 ? 2 : 4);
+  if (x != y && overlaps(x, bytes, y, bytes)) return DA_EINVAL;
+  if (da::launch_xpos(x, y, B, N, H, D, static_cast<int>(sign), transpose != 0, center, base, gamma,
+                      scale_base, static_cast<int>(dtype), static_cast<hipStream_t>(stream)) != hipSuccess)
     return DA_EHIP;
   return DA_OK;
 }

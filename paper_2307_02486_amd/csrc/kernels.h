@@ -55,4 +55,10 @@ hipError_t launch_backward(const Plan& plan, const BwdLayout& lay, const void* q
                            const void* v, const void* out, const float* lse, const void* dout, void* dq,
                            void* dk, void* dv, void* workspace, hipStream_t stream);
 
+// xPos of a [B, N, H, D] query (sign = +1) or key (sign = -1) tensor, or its
+// transpose (the backward's map), from x into y (y may equal x).
+hipError_t launch_xpos(const void* x, void* y, int64_t B, int64_t N, int64_t H, int64_t D, int sign,
+                       bool transpose, int64_t center, float base, float gamma, float scale_base,
+                       int dtype, hipStream_t stream);
+
 }  // namespace da

@@ -1,9 +1,10 @@
 """Python entry points of the dilated-attention forward and backward passes.
 
-`plan`/`dilated_attn` and `plan_bwd`/`dilated_attn_bwd` mirror the C ABI
-(dilated_attn_plan / dilated_attn_fwd, dilated_attn_bwd_plan /
-dilated_attn_bwd): torch supplies device memory and the stream, every step of
-the computation runs in the HIP kernels of libdilated_attn.so.
+`plan`/`dilated_attn`, `plan_bwd`/`dilated_attn_bwd` and `xpos` mirror the
+C ABI (dilated_attn_plan / dilated_attn_fwd, dilated_attn_bwd_plan /
+dilated_attn_bwd, dilated_attn_xpos): torch supplies device memory and the
+stream, every step of the computation runs in the HIP kernels of
+libdilated_attn.so.
 """
 from __future__ import annotations
 
@@ -173,3 +174,28 @@ def dilated_attn_bwd(q: torch.Tensor, k: torch.Tensor, v: torch.Tensor, out: tor
     if rc != 0:
         raise _lib.DilatedAttnError(rc, lib)
     return dq, dk, dv
+
+
+def xpos(x: torch.Tensor, sign: int, transpose: bool = False, center: int | None = None,
+         base: float = 10000.0, gamma: float = 0.4, scale_base: float = 512.0,
+         out: torch.Tensor | None = None, stream: torch.cuda.Stream | None = None) -> torch.Tensor:
+    """xPos of a [B, N, H, D] query (sign=+1) or key (sign=-1) tensor on the
+    GPU, or its transpose (transpose=True, the backward's map); center
+    defaults to N // 2.  `out` may be x itself.  Enqueued on `stream`."""
+    lib = _lib.load()
+    if x.device.type != "cuda":
+        raise RuntimeError("xpos runs on the GPU only; x must be a device tensor")
+    if x.dim() != 4 or not x.is_contiguous():
+        raise ValueError("x must be a contiguous [B, N, H, D] tensor")
+    B, N, H, D = x.shape
+    out = torch.empty_like(x) if out is None else out
+    if out.shape != x.shape or out.dtype != x.dtype or out.device != x.device or not out.is_contiguous():
+        raise ValueError("out must be a contiguous tensor like x")
+    if stream is None:
+        stream = torch.cuda.current_stream(x.device)
+    rc = lib.dilated_attn_xpos(x.data_ptr(), out.data_ptr(), B, N, H, D, int(sign), int(bool(transpose)),
+                               N // 2 if center is None else int(center), float(base), float(gamma),
+                               float(scale_base), _dtype_code(x.dtype), stream.cuda_stream)
+    if rc != 0:
+        raise _lib.DilatedAttnError(rc, lib)
+    return out

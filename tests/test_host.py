@@ -51,7 +51,7 @@ def test_exports_every_declared_symbol(lib):
     names = re.findall(r"^\s*(?:const\s+)?\w+\*?\s+\*?(dilated_attn_\w+)\s*\(", text, re.M)
     assert set(names) == {"dilated_attn_plan", "dilated_attn_fwd", "dilated_attn_strerror",
                           "dilated_attn_profile_begin", "dilated_attn_profile_end",
-                          "dilated_attn_bwd_plan", "dilated_attn_bwd"}
+                          "dilated_attn_bwd_plan", "dilated_attn_bwd", "dilated_attn_xpos"}
     for n in names:
         assert hasattr(lib, n), n
     nm = subprocess.run(["nm", "-D", "--defined-only", os.path.join(ROOT, "paper_2307_02486_amd",
@@ -228,3 +228,22 @@ def test_bwd_unsupported_and_errors(lib):
     assert _lib.ERRORS[call(good, ws=good[5])] == "DA_EINVAL"                     # workspace aliases dout
     assert _lib.ERRORS[call(good, D=40)] == "DA_EUNSUPPORTED"
     assert _lib.ERRORS[call(good, dtype=0)] == "DA_EUNSUPPORTED"
+
+
+@pytest.mark.parametrize("args,code", [
+    # (B, N, H, D, sign, transpose, center, base, gamma, scale_base, dtype)
+    ((1, 16, 2, 12, 1, 0, 8, 1e4, 0.4, 512.0, 1), -1),      # D not a multiple of 8
+    ((1, 16, 2, 264, 1, 0, 8, 1e4, 0.4, 512.0, 1), -1),     # D above 256
+    ((1, 16, 2, 64, 0, 0, 8, 1e4, 0.4, 512.0, 1), -1),      # sign 0
+    ((1, 16, 2, 64, 1, 2, 8, 1e4, 0.4, 512.0, 1), -1),      # transpose 2
+    ((1, 16, 2, 64, 1, 0, 16, 1e4, 0.4, 512.0, 1), -1),     # center outside [0, N)
+    ((1, 16, 2, 64, 1, 0, 8, 1.0, 0.4, 512.0, 1), -1),      # base <= 1
+    ((1, 16, 2, 64, 1, 0, 8, 1e4, 0.0, 512.0, 1), -1),      # gamma <= 0
+    ((1, 16, 2, 64, 1, 0, 8, 1e4, 0.4, float("nan"), 1), -1),
+    ((1, 40000, 1, 64, 1, 0, 20000, 1e4, 0.4, 512.0, 1), -1),  # scale exponents beyond 64
+    ((1, 16, 2, 64, 1, 0, 8, 1e4, 0.4, 512.0, 7), -2),      # unknown dtype
+    ((0, 16, 2, 64, 1, 0, 8, 1e4, 0.4, 512.0, 1), -1),
+])
+def test_xpos_rejects_bad_arguments(lib, args, code):
+    """Argument checks come before any launch: dummy pointers are never used."""
+    assert lib.dilated_attn_xpos(256, 512, *args, None) == code
