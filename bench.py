@@ -55,6 +55,10 @@ def parse():
                          "(fixed tokens per batch), one JSON line per (N, variant)")
     ap.add_argument("--backward", action="store_true",
                     help="instead of the benchmark: time the backward pass on the workload, one JSON line")
+    ap.add_argument("--layer", action="store_true",
+                    help="time the LongNet attention layer (LayerNorm, projections, xPos, dilated attention, "
+                         "sub-LayerNorm, output projection) forward and forward+backward on the workload's "
+                         "shape instead")
     ap.add_argument("--copy-calibration-mib", type=int, default=0,
                     help="only run a plain device-to-device copy of this many MiB (5 times), to "
                          "calibrate the HBM byte counters of a profiler against a known size")
@@ -288,6 +292,77 @@ def backward(args):
                                             "delta_and_sum_kernels": info["bytes_combine"]}}), flush=True)
 
 
+def layer(args):
+    """The LongNet attention layer on the workload's shape (E = H * D, bf16,
+    random-init parameters): forward, and forward + backward, per step; the
+    dilated attention's own forward and backward on the same q, k, v; and
+    the xPos kernel's bandwidth (read + write of one [B, N, H, D] tensor)."""
+    import torch
+
+    import workloads
+    from paper_2307_02486_amd import dilated_attn, dilated_attn_bwd, xpos
+    from paper_2307_02486_amd.layer import LongNetAttention
+
+    wl = workloads.BY_NAME[args.workload]
+    dev = torch.device("cuda:0")
+    torch.cuda.set_device(dev)
+    E = wl.H * wl.D
+    torch.manual_seed(0)
+    mod = LongNetAttention(E, wl.H, list(wl.patterns), wl.causal, device=dev, dtype=wl.torch_dtype)
+    x = workloads.make_random((wl.B, wl.N, E), wl.torch_dtype, 1.0, wl.seed, dev, 0).requires_grad_(True)
+    dy = workloads.make_random((wl.B, wl.N, E), wl.torch_dtype, 1.0, wl.seed, dev, 1)
+    q, k, v = workloads.make_qkv(wl, device=dev)
+    pats = list(wl.patterns)
+
+    def fwd():
+        with torch.no_grad():
+            mod(x)
+
+    def fwd_bwd():
+        mod(x).backward(dy)
+
+    def attn_fwd():
+        dilated_attn(q, k, v, pats, wl.causal)
+
+    out, lse = dilated_attn(q, k, v, pats, wl.causal)
+
+    def attn_bwd():
+        dilated_attn_bwd(q, k, v, out, lse, q, pats, wl.causal)
+
+    xo = torch.empty_like(q)
+
+    def xp():
+        xpos(q, 1, out=xo)
+
+    def timed(fn, steps):
+        t0, n = time.perf_counter(), 0
+        while n < args.warmup or time.perf_counter() - t0 < args.warmup_seconds:
+            fn()
+            n += 1
+            torch.cuda.synchronize()
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        e0.record()
+        for _ in range(steps):
+            fn()
+        e1.record()
+        torch.cuda.synchronize()
+        return e0.elapsed_time(e1) / steps
+
+    steps = max(1, args.steps)
+    ms_f, ms_fb = timed(fwd, steps), timed(fwd_bwd, steps)
+    ms_af, ms_ab = timed(attn_fwd, steps), timed(attn_bwd, steps)
+    ms_x = timed(xp, steps)
+    tok = wl.B * wl.N
+    x_bytes = 2 * q.numel() * q.element_size()
+    print(json.dumps({
+        "metric": "LongNet attention layer fwd / fwd+bwd tokens/s", "workload": wl.describe(), "embed_dim": E,
+        "dtype": wl.dtype, "steps": steps, "layer_fwd_ms": round(ms_f, 4), "layer_fwd_bwd_ms": round(ms_fb, 4),
+        "fwd_tokens_per_s": round(tok / (ms_f * 1e-3), 1), "fwd_bwd_tokens_per_s": round(tok / (ms_fb * 1e-3), 1),
+        "dilated_attn_fwd_ms": round(ms_af, 4), "dilated_attn_bwd_ms": round(ms_ab, 4),
+        "attention_share_of_fwd_bwd": round((ms_af + ms_ab) / ms_fb, 3),
+        "xpos_ms": round(ms_x, 5), "xpos_gbps": round(x_bytes / (ms_x * 1e-3) / 1e9, 1)}), flush=True)
+
+
 def main():
     args = parse()
     if args.gpus != 1:
@@ -302,6 +377,9 @@ def main():
         return
     if args.backward:
         backward(args)
+        return
+    if args.layer:
+        layer(args)
         return
     import torch
 

@@ -17,6 +17,8 @@ namespace {
 
 constexpr int kXposThreads = 256;
 constexpr double kTwoPi = 6.283185307179586476925286766559;
+constexpr double kInvTwoPi = 0.15915494309189533576888376337251;
+constexpr int kMaxPairs = 128;  // D <= 256
 
 struct XposArgs {
   const void* x;
@@ -51,27 +53,35 @@ __device__ inline void store8(unsigned short* p, const f32x8& v) {
 
 template <typename T>
 __global__ __launch_bounds__(kXposThreads) void xpos_kernel(XposArgs a) {
-  const int64_t c = static_cast<int64_t>(__builtin_amdgcn_workgroup_id_x()) * kXposThreads +
-                    __builtin_amdgcn_workitem_id_x();
+  // Per-pair constants, once per workgroup: theta_i = base^(-2i/D) in
+  // float64 (it multiplies positions of up to tens of thousands) and
+  // log2 zeta_i.
+  __shared__ double theta[kMaxPairs];
+  __shared__ float l2zeta[kMaxPairs];
+  const int tid = __builtin_amdgcn_workitem_id_x();
+  for (int i = tid; i < a.D / 2; i += kXposThreads) {
+    theta[i] = exp2(-2.0 * i / a.D * a.log2_base);
+    l2zeta[i] = log2f((2.0f * i / a.D + a.gamma) / (1.0f + a.gamma));
+  }
+  __syncthreads();
+  const int64_t c = static_cast<int64_t>(__builtin_amdgcn_workgroup_id_x()) * kXposThreads + tid;
   if (c >= a.chunks) return;
   const int per_row = a.D / 8;
-  const int64_t row = c / per_row;                   // (b, n, h) row
+  const int64_t row = c / per_row;                         // (b, n, h) row
   const int i0 = static_cast<int>(c - row * per_row) * 4;  // first pair of this thread
   const int n = static_cast<int>((row / a.H) % a.N);
-  const T* xp = static_cast<const T*>(a.x) + c * 8;
-  const f32x8 x = load8(xp);
+  const f32x8 x = load8(static_cast<const T*>(a.x) + c * 8);
   f32x8 y;
   const float rel = a.sign * static_cast<float>(n - a.center) * a.inv_scale_base;
 #pragma unroll
   for (int e = 0; e < 4; ++e) {
     const int i = i0 + e;
-    // angle n * base^(-2i/D) in float64, reduced to [-pi, pi] before the
-    // float32 sine and cosine (n * theta reaches tens of thousands of radians)
-    const double ang = static_cast<double>(n) * exp2(-2.0 * i / a.D * a.log2_base);
-    const float red = static_cast<float>(ang - kTwoPi * rint(ang / kTwoPi)) * a.angle_sign;
-    const float sn = sinf(red), cs = cosf(red);
-    const float zeta = (2.0f * i / a.D + a.gamma) / (1.0f + a.gamma);
-    const float s = exp2f(rel * log2f(zeta));
+    // angle n * theta_i in float64, reduced to [-pi, pi] before the float32
+    // sine and cosine (n * theta_0 reaches tens of thousands of radians)
+    const double ang = static_cast<double>(n) * theta[i];
+    const float red = static_cast<float>(fma(-kTwoPi, rint(ang * kInvTwoPi), ang)) * a.angle_sign;
+    const float sn = __sinf(red), cs = __cosf(red);
+    const float s = exp2f(rel * l2zeta[i]);
     const float x0 = x[2 * e], x1 = x[2 * e + 1];
     y[2 * e] = s * (x0 * cs - x1 * sn);
     y[2 * e + 1] = s * (x0 * sn + x1 * cs);
