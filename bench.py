@@ -366,7 +366,7 @@ def layer(args):
 def main():
     args = parse()
     if args.gpus != 1:
-        print(f"bench.py: this build runs on one GPU only (asked for --gpus {args.gpus}); "
+        print(f"bench.py: this benchmark runs on one GPU only (asked for --gpus {args.gpus}); "
               "the sequence-parallel multi-GPU path is not built", file=sys.stderr)
         sys.exit(2)
     if args.copy_calibration_mib > 0:

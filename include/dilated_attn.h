@@ -56,7 +56,7 @@ enum {
   DA_OK = 0,
   DA_EINVAL = -1,       /* null pointer, non-positive size, bad pattern list,
                            out aliasing an input, size beyond the limits  */
-  DA_EUNSUPPORTED = -2, /* head dim or dtype this build has no kernel for */
+  DA_EUNSUPPORTED = -2, /* head dim or dtype the library has no kernel for */
   DA_EWORKSPACE = -3,   /* workspace smaller than dilated_attn_plan asks  */
   DA_EALIGN = -4,       /* a device pointer not 16-byte aligned           */
   DA_EHIP = -5          /* the HIP runtime reported an error at launch    */
@@ -135,7 +135,7 @@ int dilated_attn_fwd(const void* q, const void* k, const void* v, void* out,
  * contributions of every pattern that keeps it (the paper's distributed
  * algorithm has this backward, Sec. 3.1).
  *
- * This build computes the backward for dtype DA_BF16 (D in {32, 64, 128});
+ * The library computes the backward for dtype DA_BF16 (D in {32, 64, 128});
  * DA_F32 returns DA_EUNSUPPORTED, and so do patterns whose dilation makes a
  * tile of 65 kept rows span 2 GiB or more (r*H*D*2*129 >= 2^31, or
  * r*4*65 >= 2^31).
