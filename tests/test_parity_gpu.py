@@ -57,6 +57,38 @@ def test_workload_sampled_rows(name):
     note(f"[parity] {name}: {len(rows)} rows, out err {eo:.3e} lse err {el:.3e}")
 
 
+@pytest.mark.parametrize("name", ["n32k_h12_d64_5pat", "n8k_b2_h12_d64_3pat"])
+def test_non_causal_sampled_rows(name):
+    """The workloads' shapes with causal = False (Eq. 6 literally: every kept
+    key of the segment is visible)."""
+    import dataclasses
+    wl = dataclasses.replace(workloads.BY_NAME[name], causal=False)
+    note(f"[parity] {name} non-causal sampled rows")
+    q, k, v = workloads.make_qkv(wl, device="cuda")
+    out, lse = run_gpu(q, k, v, list(wl.patterns), False)
+    assert torch.isfinite(lse).all().item() and torch.isfinite(out).all().item()
+    rows = sample_rows(wl, np.random.default_rng(wl.seed + 1), per_head=24)
+    eo, el = compare_rows(q, k, v, out, lse, wl, rows, tag=name + " non-causal")
+    note(f"[parity] {name} non-causal: {len(rows)} rows, out err {eo:.3e} lse err {el:.3e}")
+
+
+WIDER = [
+    # (B, N, H, D, dtype, patterns, causal): longer segments than the edge cases
+    (1, 4096, 4, 64, "f32", [(2048, 1), (4096, 4)], True),      # float32 kernel, 32 query tiles per segment
+    (2, 8192, 8, 32, "bf16", [(2048, 1), (4096, 2), (8192, 4)], True),  # D = 32 at the 8K shape
+]
+
+
+@pytest.mark.parametrize("case", WIDER, ids=lambda c: f"B{c[0]}N{c[1]}H{c[2]}D{c[3]}{c[4]}")
+def test_wider_cases_all_rows(case):
+    B, N, H, D, dt, pats, causal = case
+    note(f"[wider] {case}")
+    dtype = torch.bfloat16 if dt == "bf16" else torch.float32
+    q, k, v = (workloads.make_random((B, N, H, D), dtype, 1.0, 2000 + N + D, "cuda", t) for t in range(3))
+    eo, el = compare_full(q, k, v, pats, causal, dt, tag=str(case))
+    note(f"[wider] {case}: out err {eo:.3e} lse err {el:.3e}")
+
+
 # ---- edge cases at small sizes ------------------------------------------------
 
 EDGE = [
