@@ -300,7 +300,7 @@ def layer(args):
     import torch
 
     import workloads
-    from paper_2307_02486_amd import dilated_attn, dilated_attn_bwd, xpos
+    from paper_2307_02486_amd import dilated_attn, dilated_attn_bwd, wgrad, xpos
     from paper_2307_02486_amd.layer import LongNetAttention
 
     wl = workloads.BY_NAME[args.workload]
@@ -334,6 +334,15 @@ def layer(args):
     def xp():
         xpos(q, 1, out=xo)
 
+    dy2, x2 = dy.view(-1, E), x.detach().view(-1, E)
+    wo = torch.empty((E, E), dtype=dy.dtype, device=dev)
+
+    def wg():
+        wgrad(dy2, x2, out=wo)
+
+    def wg_torch():
+        torch.mm(dy2.t(), x2)
+
     def timed(fn, steps):
         t0, n = time.perf_counter(), 0
         while n < args.warmup or time.perf_counter() - t0 < args.warmup_seconds:
@@ -352,7 +361,9 @@ def layer(args):
     ms_f, ms_fb = timed(fwd, steps), timed(fwd_bwd, steps)
     ms_af, ms_ab = timed(attn_fwd, steps), timed(attn_bwd, steps)
     ms_x = timed(xp, steps)
+    ms_w, ms_wt = timed(wg, steps), timed(wg_torch, steps)
     tok = wl.B * wl.N
+    w_flop = 2.0 * tok * E * E
     x_bytes = 2 * q.numel() * q.element_size()
     print(json.dumps({
         "metric": "LongNet attention layer fwd / fwd+bwd tokens/s", "workload": wl.describe(), "embed_dim": E,
@@ -360,7 +371,9 @@ def layer(args):
         "fwd_tokens_per_s": round(tok / (ms_f * 1e-3), 1), "fwd_bwd_tokens_per_s": round(tok / (ms_fb * 1e-3), 1),
         "dilated_attn_fwd_ms": round(ms_af, 4), "dilated_attn_bwd_ms": round(ms_ab, 4),
         "attention_share_of_fwd_bwd": round((ms_af + ms_ab) / ms_fb, 3),
-        "xpos_ms": round(ms_x, 5), "xpos_gbps": round(x_bytes / (ms_x * 1e-3) / 1e9, 1)}), flush=True)
+        "xpos_ms": round(ms_x, 5), "xpos_gbps": round(x_bytes / (ms_x * 1e-3) / 1e9, 1),
+        "wgrad_ms": round(ms_w, 5), "wgrad_tflops": round(w_flop / (ms_w * 1e-3) / 1e12, 1),
+        "torch_mm_wgrad_ms": round(ms_wt, 5)}), flush=True)
 
 
 def main():

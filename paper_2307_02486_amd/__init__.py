@@ -5,8 +5,8 @@ The computation runs in the HIP kernels of libdilated_attn.so behind the C
 ABI declared in include/dilated_attn.h; this package only marshals arguments.
 """
 from .ops import (StageTimer, bwd_workspace_for, dilated_attn, dilated_attn_bwd, plan,  # noqa: F401
-                  plan_bwd, plan_raw, workspace_for, xpos)
+                  plan_bwd, plan_raw, wgrad, workspace_for, xpos)
 from ._lib import DilatedAttnError, LIB_PATH  # noqa: F401
 
 __all__ = ["StageTimer", "dilated_attn", "dilated_attn_bwd", "plan", "plan_bwd", "plan_raw",
-           "workspace_for", "bwd_workspace_for", "xpos", "DilatedAttnError", "LIB_PATH"]
+           "workspace_for", "bwd_workspace_for", "xpos", "wgrad", "DilatedAttnError", "LIB_PATH"]

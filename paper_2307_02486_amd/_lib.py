@@ -70,6 +70,10 @@ def load():
     lib.dilated_attn_bwd.restype = ctypes.c_int
     lib.dilated_attn_xpos.argtypes = [vp, vp, i64, i64, i64, i64, i64, i64, i64, f32, f32, f32, i64, vp]
     lib.dilated_attn_xpos.restype = ctypes.c_int
+    lib.dilated_attn_wgrad_workspace.argtypes = [i64, i64, i64, ctypes.POINTER(ctypes.c_uint64)]
+    lib.dilated_attn_wgrad_workspace.restype = ctypes.c_int
+    lib.dilated_attn_wgrad.argtypes = [vp, vp, vp, i64, i64, i64, i64, vp, ctypes.c_uint64, vp]
+    lib.dilated_attn_wgrad.restype = ctypes.c_int
     lib.dilated_attn_strerror.argtypes = [ctypes.c_int]
     lib.dilated_attn_strerror.restype = ctypes.c_char_p
     lib.dilated_attn_profile_begin.argtypes = [i64]

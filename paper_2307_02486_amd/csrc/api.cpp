@@ -195,6 +195,36 @@ int dilated_attn_xpos(const void* x, void* y, int64_t B, int64_t N, int64_t H, i
   return DA_OK;
 }
 
+int dilated_attn_wgrad_workspace(int64_t K, int64_t M, int64_t N, uint64_t* bytes) {
+  if (!bytes) return DA_EINVAL;
+  if (K < 0 || K > (int64_t{1} << 30) || M <= 0 || N <= 0 || M % 128 || N % 128 || M > 16384 || N > 16384)
+    return DA_EINVAL;
+  int64_t chunk = 0;
+  *bytes = static_cast<uint64_t>(da::wgrad_splits(K, M, N, &chunk)) * M * N * 4;
+  return DA_OK;
+}
+
+int dilated_attn_wgrad(const void* dy, const void* x, void* dw, int64_t K, int64_t M, int64_t N,
+                       int64_t dtype, void* workspace, uint64_t workspace_bytes, void* stream) {
+  uint64_t need = 0;
+  if (!dw || (K > 0 && (!dy || !x))) return DA_EINVAL;
+  if (dilated_attn_wgrad_workspace(K, M, N, &need) != DA_OK) return DA_EINVAL;
+  if (dtype != DA_BF16) return DA_EUNSUPPORTED;
+  if (need > 0 && !workspace) return DA_EINVAL;
+  if (!aligned16(dy) || !aligned16(x) || !aligned16(dw) || (need > 0 && !aligned16(workspace)))
+    return DA_EALIGN;
+  if (workspace_bytes < need) return DA_EWORKSPACE;
+  const uint64_t dwb = static_cast<uint64_t>(M * N) * 2;
+  if (overlaps(dw, dwb, dy, static_cast<uint64_t>(K * M) * 2) || overlaps(dw, dwb, x, static_cast<uint64_t>(K * N) * 2))
+    return DA_EINVAL;
+  if (need > 0 && (overlaps(workspace, need, dw, dwb) || overlaps(workspace, need, dy, static_cast<uint64_t>(K * M) * 2) ||
+                   overlaps(workspace, need, x, static_cast<uint64_t>(K * N) * 2)))
+    return DA_EINVAL;
+  if (da::launch_wgrad(dy, x, dw, K, M, N, workspace, static_cast<hipStream_t>(stream)) != hipSuccess)
+    return DA_EHIP;
+  return DA_OK;
+}
+
 int dilated_attn_profile_begin(int64_t capacity) {
   if (g_prof.active || capacity < 1 || capacity > (int64_t{1} << 20)) return DA_EINVAL;
   g_prof.ev.assign(static_cast<size_t>(3 * capacity), nullptr);

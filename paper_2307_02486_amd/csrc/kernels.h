@@ -61,4 +61,10 @@ hipError_t launch_xpos(const void* x, void* y, int64_t B, int64_t N, int64_t H, 
                        bool transpose, int64_t center, float base, float gamma, float scale_base,
                        int dtype, hipStream_t stream);
 
+// Weight gradient dw[M][N] = sum_k dy[k][M] x[k][N] (bf16, M and N multiples
+// of 128): float32 partial sums over k-chunks in workspace, then their sum.
+int64_t wgrad_splits(int64_t K, int64_t M, int64_t N, int64_t* chunk);
+hipError_t launch_wgrad(const void* dy, const void* x, void* dw, int64_t K, int64_t M, int64_t N, void* workspace,
+                        hipStream_t stream);
+
 }  // namespace da

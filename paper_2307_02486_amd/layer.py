@@ -10,8 +10,10 @@ the standard attention replaced by dilated attention).
 
 The residual connection belongs to the block around the layer.  The
 attention and xPos run in the library's HIP kernels (their backward passes
-too); the projections and LayerNorms are plain library GEMMs and
-normalisations from torch.
+too), and so do the projections' weight gradients in bf16 (dilated_attn_wgrad:
+a long reduction over B * N rows into a small E x E matrix, a shape that
+general GEMM libraries split poorly); the other products and the LayerNorms
+are plain library GEMMs and normalisations from torch.
 """
 from __future__ import annotations
 
@@ -19,7 +21,7 @@ from typing import Sequence, Tuple
 
 import torch
 
-from .ops import dilated_attn, dilated_attn_bwd, xpos
+from .ops import dilated_attn, dilated_attn_bwd, wgrad, xpos
 
 
 class DilatedAttentionFunction(torch.autograd.Function):
@@ -55,6 +57,33 @@ class XPosFunction(torch.autograd.Function):
         return xpos(dy.contiguous(), sign, True, center, base, gamma, scale_base), None, None, None, None, None
 
 
+class LinearFunction(torch.autograd.Function):
+    """y = x w^T + b over the last dimension, with dw = dy^T x from the
+    library's weight-gradient kernel when it applies (bf16, both dimensions
+    multiples of 128) and from torch's GEMM otherwise."""
+
+    @staticmethod
+    def forward(ctx, x, w, b):
+        ctx.save_for_backward(x, w)
+        return torch.nn.functional.linear(x, w, b)
+
+    @staticmethod
+    def backward(ctx, dy):
+        x, w = ctx.saved_tensors
+        dy2 = dy.reshape(-1, dy.shape[-1]).contiguous()
+        x2 = x.reshape(-1, x.shape[-1]).contiguous()
+        dx = (dy2 @ w).view(x.shape)
+        if dy2.dtype == torch.bfloat16 and dy2.shape[1] % 128 == 0 and x2.shape[1] % 128 == 0:
+            dw = wgrad(dy2, x2)
+        else:
+            dw = dy2.t() @ x2
+        return dx, dw, dy2.sum(0)
+
+
+def _linear(mod: torch.nn.Linear, x: torch.Tensor) -> torch.Tensor:
+    return LinearFunction.apply(x, mod.weight, mod.bias)
+
+
 class LongNetAttention(torch.nn.Module):
     """Attention sublayer with dilated attention (see the module docstring).
 
@@ -88,15 +117,15 @@ class LongNetAttention(torch.nn.Module):
         B, N, E = x.shape
         H, D = self.num_heads, self.head_dim
         u = self.ln_in(x)
-        q = self.q_proj(u).view(B, N, H, D)
-        k = self.k_proj(u).view(B, N, H, D)
-        v = self.v_proj(u).view(B, N, H, D)
+        q = _linear(self.q_proj, u).view(B, N, H, D)
+        k = _linear(self.k_proj, u).view(B, N, H, D)
+        v = _linear(self.v_proj, u).view(B, N, H, D)
         if self.use_xpos:
             base, gamma, scale_base = self.xpos_args
             q = XPosFunction.apply(q, 1, N // 2, base, gamma, scale_base)
             k = XPosFunction.apply(k, -1, N // 2, base, gamma, scale_base)
         a = DilatedAttentionFunction.apply(q, k, v, self.patterns, self.causal, None)
-        return self.out_proj(self.ln_sub(a.reshape(B, N, E)))
+        return _linear(self.out_proj, self.ln_sub(a.reshape(B, N, E)))
 
     def float64_params(self) -> dict:
         """The parameters as float64 NumPy arrays, keyed ln_in_g, ln_in_b, wq,

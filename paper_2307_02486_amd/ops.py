@@ -199,3 +199,34 @@ def xpos(x: torch.Tensor, sign: int, transpose: bool = False, center: int | None
     if rc != 0:
         raise _lib.DilatedAttnError(rc, lib)
     return out
+
+
+def wgrad(dy: torch.Tensor, x: torch.Tensor, out: torch.Tensor | None = None,
+          stream: torch.cuda.Stream | None = None) -> torch.Tensor:
+    """dw = dy^T x for bf16 dy [K, M] and x [K, N] on the GPU (M, N multiples
+    of 128): the weight gradient of a projection y = x w^T.  Enqueued on
+    `stream`; the float32 workspace comes from torch's caching allocator."""
+    lib = _lib.load()
+    if dy.device.type != "cuda" or x.device != dy.device:
+        raise RuntimeError("wgrad runs on the GPU only; dy and x must be tensors of one device")
+    if dy.dim() != 2 or x.dim() != 2 or dy.shape[0] != x.shape[0] or not dy.is_contiguous() \
+            or not x.is_contiguous() or x.dtype != dy.dtype:
+        raise ValueError("dy [K, M] and x [K, N] must be contiguous 2-D tensors of one dtype")
+    K, M = dy.shape
+    N = x.shape[1]
+    need = ctypes.c_uint64(0)
+    rc = lib.dilated_attn_wgrad_workspace(K, M, N, ctypes.byref(need))
+    if rc != 0:
+        raise _lib.DilatedAttnError(rc, lib)
+    out = torch.empty((M, N), dtype=dy.dtype, device=dy.device) if out is None else out
+    if out.shape != (M, N) or out.dtype != dy.dtype or out.device != dy.device or not out.is_contiguous():
+        raise ValueError("out must be a contiguous [M, N] tensor of dy's dtype")
+    ws = torch.empty(max(need.value, 16), dtype=torch.uint8, device=dy.device)
+    if stream is None:
+        stream = torch.cuda.current_stream(dy.device)
+    rc = lib.dilated_attn_wgrad(dy.data_ptr(), x.data_ptr(), out.data_ptr(), K, M, N, _dtype_code(dy.dtype),
+                                ws.data_ptr(), need.value, stream.cuda_stream)
+    if rc != 0:
+        raise _lib.DilatedAttnError(rc, lib)
+    ws.record_stream(stream)
+    return out

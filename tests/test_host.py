@@ -51,7 +51,8 @@ def test_exports_every_declared_symbol(lib):
     names = re.findall(r"^\s*(?:const\s+)?\w+\*?\s+\*?(dilated_attn_\w+)\s*\(", text, re.M)
     assert set(names) == {"dilated_attn_plan", "dilated_attn_fwd", "dilated_attn_strerror",
                           "dilated_attn_profile_begin", "dilated_attn_profile_end",
-                          "dilated_attn_bwd_plan", "dilated_attn_bwd", "dilated_attn_xpos"}
+                          "dilated_attn_bwd_plan", "dilated_attn_bwd", "dilated_attn_xpos",
+                          "dilated_attn_wgrad_workspace", "dilated_attn_wgrad"}
     for n in names:
         assert hasattr(lib, n), n
     nm = subprocess.run(["nm", "-D", "--defined-only", os.path.join(ROOT, "paper_2307_02486_amd",
@@ -247,3 +248,38 @@ def test_bwd_unsupported_and_errors(lib):
 def test_xpos_rejects_bad_arguments(lib, args, code):
     """Argument checks come before any launch: dummy pointers are never used."""
     assert lib.dilated_attn_xpos(256, 512, *args, None) == code
+
+
+def test_wgrad_workspace_sizes(lib):
+    """Splits of the reduction: at most 512 workgroups of 128 x 128 output
+    tiles, whole 64-row k tiles per split, none for an empty reduction."""
+    import ctypes
+    out = ctypes.c_uint64(0)
+
+    def ws(K, M, N):
+        rc = lib.dilated_attn_wgrad_workspace(K, M, N, ctypes.byref(out))
+        return rc if rc else out.value
+
+    assert ws(0, 768, 768) == 0
+    assert ws(1, 768, 768) == 768 * 768 * 4                 # one k tile: one split
+    assert ws(32768, 768, 768) == 14 * 768 * 768 * 4       # 36 tiles x 14 splits = 504 workgroups
+    assert ws(64 * 100, 128, 128) == 100 * 128 * 128 * 4    # 512 splits capped at the 100 k tiles
+    assert ws(1 << 20, 16384, 16384) == 16384 * 16384 * 4   # more tiles than 512: one split
+    for bad in ((-1, 128, 128), (64, 100, 128), (64, 128, 0), (64, 128, 16512), ((1 << 30) + 1, 128, 128)):
+        assert ws(*bad) == -1, bad
+
+
+@pytest.mark.parametrize("args,code", [
+    # (K, M, N, dtype, workspace, workspace_bytes)
+    ((64, 100, 128, 1, 4096, 1 << 20), -1),          # M not a multiple of 128
+    ((64, 128, 128, 0, 4096, 1 << 20), -2),          # float32: no kernel
+    ((64, 128, 128, 1, 4096, 16), -3),               # workspace too small
+    ((64, 128, 128, 1, None, 1 << 20), -1),          # no workspace
+    ((64, 128, 128, 1, 4100, 1 << 20), -4),          # workspace misaligned
+    ((64, 128, 128, 1, 512, 1 << 20), -1),           # workspace overlaps x
+])
+def test_wgrad_rejects_bad_arguments(lib, args, code):
+    """Argument checks come before any launch: dummy pointers are never used.
+    dy at 256, x at 512 and dw at 1 << 24 (sizes small enough not to meet)."""
+    K, M, N, dtype, ws, wsb = args
+    assert lib.dilated_attn_wgrad(256, 512, 1 << 24, K, M, N, dtype, ws, wsb, None) == code
