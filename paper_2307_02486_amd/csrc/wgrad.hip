@@ -30,6 +30,7 @@ struct WgradArgs {
   float* part;     // [splits][M][N]
   int64_t K;
   int32_t M, N, chunk, tiles_n, tiles;
+  int32_t items, per_xcd;  // tiles * splits, and items per XCD (rounded up)
 };
 
 struct SmemWgrad {
@@ -43,8 +44,14 @@ __global__ __launch_bounds__(kWgThreads) void wgrad_partial(WgradArgs a) {
   const int lane = tid & 63;
   const int wv = __builtin_amdgcn_readfirstlane(tid >> 6);
   const int hi = lane >> 5;
+  // Workgroup i runs on XCD i % 8.  Item (split, tile) = split * tiles + tile
+  // goes to workgroup (item % per) * 8 + item / per, so that XCD x takes items
+  // [x per, (x + 1) per): the tiles of one or two neighbouring k-chunks, whose
+  // rows its own L2 then serves to every tile after the first fetch.
   const int blk = __builtin_amdgcn_workgroup_id_x();
-  const int tile = blk % a.tiles, split = blk / a.tiles;
+  const int item = (blk & 7) * a.per_xcd + (blk >> 3);
+  if (item >= a.items) return;
+  const int tile = item % a.tiles, split = item / a.tiles;
   const int m0 = (tile / a.tiles_n) * kTileMN, n0 = (tile % a.tiles_n) * kTileMN;
   const int64_t k0 = static_cast<int64_t>(split) * a.chunk;
   const int64_t k1 = k0 + a.chunk < a.K ? k0 + a.chunk : a.K;
@@ -194,9 +201,10 @@ hipError_t launch_wgrad(const void* dy, const void* x, void* dw, int64_t K, int6
   a.chunk = static_cast<int32_t>(chunk);
   a.tiles_n = static_cast<int32_t>(N / kTileMN);
   a.tiles = static_cast<int32_t>((M / kTileMN) * (N / kTileMN));
+  a.items = static_cast<int32_t>(a.tiles * splits);
+  a.per_xcd = (a.items + 7) / 8;
   if (splits > 0)
-    hipLaunchKernelGGL(wgrad_partial, dim3(static_cast<unsigned>(a.tiles * splits)), dim3(kWgThreads), 0, stream,
-                       a);
+    hipLaunchKernelGGL(wgrad_partial, dim3(static_cast<unsigned>(8 * a.per_xcd)), dim3(kWgThreads), 0, stream, a);
   const int64_t mn = M * N;
   hipLaunchKernelGGL(wgrad_sum, dim3(static_cast<unsigned>((mn / 4 + kWgThreads - 1) / kWgThreads)),
                      dim3(kWgThreads), 0, stream, static_cast<const float*>(workspace), static_cast<u16*>(dw), mn,
