@@ -248,6 +248,62 @@ int dilated_attn_wgrad_workspace(int64_t K, int64_t M, int64_t N, uint64_t* byte
 int dilated_attn_wgrad(const void* dy, const void* x, void* dw, int64_t K, int64_t M, int64_t N,
                        int64_t dtype, void* workspace, uint64_t workspace_bytes, void* stream);
 
+/*
+ * dilated_attn_layernorm_fwd - LayerNorm of the layer around the dilated
+ * attention (the input LayerNorm and Magneto's sub-LayerNorm of the paper's
+ * language model, Sec. 4.1), over rows of E elements:
+ *   mean = sum(x) / E,  rstd = 1 / sqrt(sum((x - mean)^2) / E + eps),
+ *   y = (x - mean) * rstd * g + b.
+ *
+ * x, y        device pointers, [rows, E] bf16 row-major, 16-byte aligned; y may
+ *             equal x (in place) but must not overlap it otherwise.  x may be
+ *             NULL when rows = 0.
+ * g, b        device pointers, [E] bf16, 16-byte aligned.
+ * mean, rstd  device pointers, [rows] float32 (outputs, kept for the backward).
+ * rows        0 <= rows <= 2^31.
+ * E           a multiple of 8, 8 <= E <= 2048.
+ * eps         finite, > 0.
+ * dtype       DA_BF16 (others: DA_EUNSUPPORTED).
+ * stream      a hipStream_t (NULL = the default stream); asynchronous.
+ *
+ * Statistics and arithmetic in float32, y rounded to bf16.  Outputs must not
+ * overlap each other, g, b or (mean, rstd) x.  Returns DA_OK or a negative
+ * code; errors launch nothing.
+ */
+int dilated_attn_layernorm_fwd(const void* x, const void* g, const void* b, void* y, float* mean,
+                               float* rstd, int64_t rows, int64_t E, float eps, int64_t dtype,
+                               void* stream);
+
+/*
+ * dilated_attn_layernorm_bwd - gradients of dilated_attn_layernorm_fwd given
+ * the incoming gradient dy and the forward's saved mean and rstd: with
+ * xhat = (x - mean) * rstd and dxhat = dy * g,
+ *   dx = rstd * (dxhat - mean_row(dxhat) - xhat * mean_row(dxhat * xhat)),
+ *   dg = sum over rows of dy * xhat,  db = sum over rows of dy.
+ *
+ * dy, x       device pointers, [rows, E] bf16, 16-byte aligned.
+ * g           device pointer, [E] bf16, 16-byte aligned.
+ * mean, rstd  device pointers, [rows] float32 from the forward call.
+ * dx          device pointer, [rows, E] bf16 (output).
+ * dg, db      device pointers, [E] bf16 (outputs; zeros when rows = 0).
+ * rows, E     as for the forward.
+ * workspace   device scratch of at least the bytes that
+ *             dilated_attn_layernorm_bwd_workspace reports, owned by the
+ *             caller, 16-byte aligned; contents on entry ignored, on return
+ *             unspecified.
+ * stream      a hipStream_t (NULL = the default stream); asynchronous.
+ *
+ * Float32 arithmetic; dg and db summed per 64 rows and then over those sums
+ * in a fixed order (the result does not depend on scheduling), rounded to
+ * bf16 once.  Outputs and workspace must not overlap each other or any
+ * input.  Returns DA_OK or a negative code; errors launch nothing.
+ */
+int dilated_attn_layernorm_bwd_workspace(int64_t rows, int64_t E, uint64_t* bytes);
+int dilated_attn_layernorm_bwd(const void* dy, const void* x, const void* g, const float* mean,
+                               const float* rstd, void* dx, void* dg, void* db, int64_t rows,
+                               int64_t E, int64_t dtype, void* workspace, uint64_t workspace_bytes,
+                               void* stream);
+
 /* Human-readable text for an error code (static storage, never NULL). */
 const char* dilated_attn_strerror(int code);
 

@@ -4,9 +4,9 @@ Sec. 2.2-2.3).
 The computation runs in the HIP kernels of libdilated_attn.so behind the C
 ABI declared in include/dilated_attn.h; this package only marshals arguments.
 """
-from .ops import (StageTimer, bwd_workspace_for, dilated_attn, dilated_attn_bwd, plan,  # noqa: F401
-                  plan_bwd, plan_raw, wgrad, workspace_for, xpos)
+from .ops import (StageTimer, bwd_workspace_for, dilated_attn, dilated_attn_bwd, layer_norm,  # noqa: F401
+                  layer_norm_bwd, plan, plan_bwd, plan_raw, wgrad, workspace_for, xpos)
 from ._lib import DilatedAttnError, LIB_PATH  # noqa: F401
 
 __all__ = ["StageTimer", "dilated_attn", "dilated_attn_bwd", "plan", "plan_bwd", "plan_raw",
-           "workspace_for", "bwd_workspace_for", "xpos", "wgrad", "DilatedAttnError", "LIB_PATH"]
+           "workspace_for", "bwd_workspace_for", "xpos", "wgrad", "layer_norm", "layer_norm_bwd", "DilatedAttnError", "LIB_PATH"]

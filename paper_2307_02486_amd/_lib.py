@@ -74,6 +74,12 @@ def load():
     lib.dilated_attn_wgrad_workspace.restype = ctypes.c_int
     lib.dilated_attn_wgrad.argtypes = [vp, vp, vp, i64, i64, i64, i64, vp, ctypes.c_uint64, vp]
     lib.dilated_attn_wgrad.restype = ctypes.c_int
+    lib.dilated_attn_layernorm_fwd.argtypes = [vp, vp, vp, vp, vp, vp, i64, i64, f32, i64, vp]
+    lib.dilated_attn_layernorm_fwd.restype = ctypes.c_int
+    lib.dilated_attn_layernorm_bwd_workspace.argtypes = [i64, i64, ctypes.POINTER(ctypes.c_uint64)]
+    lib.dilated_attn_layernorm_bwd_workspace.restype = ctypes.c_int
+    lib.dilated_attn_layernorm_bwd.argtypes = [vp, vp, vp, vp, vp, vp, vp, vp, i64, i64, i64, vp, ctypes.c_uint64, vp]
+    lib.dilated_attn_layernorm_bwd.restype = ctypes.c_int
     lib.dilated_attn_strerror.argtypes = [ctypes.c_int]
     lib.dilated_attn_strerror.restype = ctypes.c_char_p
     lib.dilated_attn_profile_begin.argtypes = [i64]

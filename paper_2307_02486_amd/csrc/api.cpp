@@ -225,6 +225,64 @@ int dilated_attn_wgrad(const void* dy, const void* x, void* dw, int64_t K, int64
   return DA_OK;
 }
 
+int dilated_attn_layernorm_fwd(const void* x, const void* g, const void* b, void* y, float* mean, float* rstd,
+                               int64_t rows, int64_t E, float eps, int64_t dtype, void* stream) {
+  if (!g || !b || !y || !mean || !rstd || (rows > 0 && !x)) return DA_EINVAL;
+  if (rows < 0 || rows > (int64_t{1} << 31) || E < 8 || E > 2048 || E % 8 || !std::isfinite(eps) || !(eps > 0.0f))
+    return DA_EINVAL;
+  if (dtype != DA_BF16) return DA_EUNSUPPORTED;
+  if (!aligned16(x) || !aligned16(g) || !aligned16(b) || !aligned16(y)) return DA_EALIGN;
+  const uint64_t xb = static_cast<uint64_t>(rows * E) * 2, sb = static_cast<uint64_t>(rows) * 4;
+  if (x != y && overlaps(x, xb, y, xb)) return DA_EINVAL;
+  const void* outs[3] = {y, mean, rstd};
+  const uint64_t osz[3] = {xb, sb, sb};
+  for (int i = 0; i < 3; ++i) {
+    for (int j = i + 1; j < 3; ++j)
+      if (overlaps(outs[i], osz[i], outs[j], osz[j])) return DA_EINVAL;
+    if (overlaps(outs[i], osz[i], g, static_cast<uint64_t>(E) * 2) ||
+        overlaps(outs[i], osz[i], b, static_cast<uint64_t>(E) * 2))
+      return DA_EINVAL;
+  }
+  if (overlaps(mean, sb, x, xb) || overlaps(rstd, sb, x, xb)) return DA_EINVAL;
+  if (da::launch_layernorm_fwd(x, g, b, y, mean, rstd, rows, E, eps, static_cast<hipStream_t>(stream)) !=
+      hipSuccess)
+    return DA_EHIP;
+  return DA_OK;
+}
+
+int dilated_attn_layernorm_bwd_workspace(int64_t rows, int64_t E, uint64_t* bytes) {
+  if (!bytes || rows < 0 || rows > (int64_t{1} << 31) || E < 8 || E > 2048 || E % 8) return DA_EINVAL;
+  *bytes = da::layernorm_bwd_workspace(rows, E);
+  return DA_OK;
+}
+
+int dilated_attn_layernorm_bwd(const void* dy, const void* x, const void* g, const float* mean, const float* rstd,
+                               void* dx, void* dg, void* db, int64_t rows, int64_t E, int64_t dtype,
+                               void* workspace, uint64_t workspace_bytes, void* stream) {
+  uint64_t need = 0;
+  if (dilated_attn_layernorm_bwd_workspace(rows, E, &need) != DA_OK) return DA_EINVAL;
+  if (!g || !dg || !db || !workspace || (rows > 0 && (!dy || !x || !mean || !rstd || !dx))) return DA_EINVAL;
+  if (dtype != DA_BF16) return DA_EUNSUPPORTED;
+  if (!aligned16(dy) || !aligned16(x) || !aligned16(g) || !aligned16(dx) || !aligned16(workspace)) return DA_EALIGN;
+  if (workspace_bytes < need) return DA_EWORKSPACE;
+  const uint64_t xb = static_cast<uint64_t>(rows * E) * 2, sb = static_cast<uint64_t>(rows) * 4,
+                 eb = static_cast<uint64_t>(E) * 2;
+  const void* ins[5] = {dy, x, g, mean, rstd};
+  const uint64_t isz[5] = {xb, xb, eb, sb, sb};
+  const void* outs[4] = {dx, dg, db, workspace};
+  const uint64_t osz[4] = {xb, eb, eb, need};
+  for (int i = 0; i < 4; ++i) {
+    for (int j = i + 1; j < 4; ++j)
+      if (overlaps(outs[i], osz[i], outs[j], osz[j])) return DA_EINVAL;
+    for (int j = 0; j < 5; ++j)
+      if (overlaps(outs[i], osz[i], ins[j], isz[j])) return DA_EINVAL;
+  }
+  if (da::launch_layernorm_bwd(dy, x, g, mean, rstd, dx, dg, db, rows, E, workspace,
+                               static_cast<hipStream_t>(stream)) != hipSuccess)
+    return DA_EHIP;
+  return DA_OK;
+}
+
 int dilated_attn_profile_begin(int64_t capacity) {
   if (g_prof.active || capacity < 1 || capacity > (int64_t{1} << 20)) return DA_EINVAL;
   g_prof.ev.assign(static_cast<size_t>(3 * capacity), nullptr);

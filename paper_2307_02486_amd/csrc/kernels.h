@@ -67,4 +67,14 @@ int64_t wgrad_splits(int64_t K, int64_t M, int64_t N, int64_t* chunk);
 hipError_t launch_wgrad(const void* dy, const void* x, void* dw, int64_t K, int64_t M, int64_t N, void* workspace,
                         hipStream_t stream);
 
+// LayerNorm over rows of E bf16 elements (E a multiple of 8, at most 2048),
+// float32 statistics; the backward's parameter gradients go through a
+// float32 workspace of layernorm_bwd_workspace(rows, E) bytes.
+hipError_t launch_layernorm_fwd(const void* x, const void* g, const void* b, void* y, float* mean, float* rstd,
+                                int64_t rows, int64_t E, float eps, hipStream_t stream);
+uint64_t layernorm_bwd_workspace(int64_t rows, int64_t E);
+hipError_t launch_layernorm_bwd(const void* dy, const void* x, const void* g, const float* mean, const float* rstd,
+                                void* dx, void* dg, void* db, int64_t rows, int64_t E, void* workspace,
+                                hipStream_t stream);
+
 }  // namespace da

@@ -10,10 +10,11 @@ the standard attention replaced by dilated attention).
 
 The residual connection belongs to the block around the layer.  The
 attention and xPos run in the library's HIP kernels (their backward passes
-too), and so do the projections' weight gradients in bf16 (dilated_attn_wgrad:
-a long reduction over B * N rows into a small E x E matrix, a shape that
-general GEMM libraries split poorly); the other products and the LayerNorms
-are plain library GEMMs and normalisations from torch.
+too), and so do, in bf16, the LayerNorms (dilated_attn_layernorm_fwd / _bwd)
+and the projections' weight gradients (dilated_attn_wgrad: a long reduction
+over B * N rows into a small E x E matrix, a shape that general GEMM
+libraries split poorly); the other products are plain library GEMMs from
+torch.
 """
 from __future__ import annotations
 
@@ -21,7 +22,7 @@ from typing import Sequence, Tuple
 
 import torch
 
-from .ops import dilated_attn, dilated_attn_bwd, wgrad, xpos
+from .ops import dilated_attn, dilated_attn_bwd, layer_norm, layer_norm_bwd, wgrad, xpos
 
 
 class DilatedAttentionFunction(torch.autograd.Function):
@@ -84,6 +85,31 @@ def _linear(mod: torch.nn.Linear, x: torch.Tensor) -> torch.Tensor:
     return LinearFunction.apply(x, mod.weight, mod.bias)
 
 
+class LayerNormFunction(torch.autograd.Function):
+    """LayerNorm over the last dimension through the library's kernels."""
+
+    @staticmethod
+    def forward(ctx, x, weight, bias, eps):
+        x = x.contiguous()
+        y, mean, rstd = layer_norm(x, weight, bias, eps)
+        ctx.save_for_backward(x, weight, mean, rstd)
+        return y
+
+    @staticmethod
+    def backward(ctx, dy):
+        x, weight, mean, rstd = ctx.saved_tensors
+        dx, dw, db = layer_norm_bwd(dy.contiguous(), x, weight, mean, rstd)
+        return dx, dw, db, None
+
+
+def _layer_norm(mod: torch.nn.LayerNorm, x: torch.Tensor) -> torch.Tensor:
+    """The library's LayerNorm for bf16 rows of E <= 2048 (E % 8 == 0), torch's otherwise."""
+    E = x.shape[-1]
+    if x.dtype == torch.bfloat16 and E % 8 == 0 and E <= 2048:
+        return LayerNormFunction.apply(x, mod.weight, mod.bias, mod.eps)
+    return mod(x)
+
+
 class LongNetAttention(torch.nn.Module):
     """Attention sublayer with dilated attention (see the module docstring).
 
@@ -116,7 +142,7 @@ class LongNetAttention(torch.nn.Module):
     def forward(self, x: torch.Tensor) -> torch.Tensor:
         B, N, E = x.shape
         H, D = self.num_heads, self.head_dim
-        u = self.ln_in(x)
+        u = _layer_norm(self.ln_in, x)
         q = _linear(self.q_proj, u).view(B, N, H, D)
         k = _linear(self.k_proj, u).view(B, N, H, D)
         v = _linear(self.v_proj, u).view(B, N, H, D)
@@ -125,7 +151,7 @@ class LongNetAttention(torch.nn.Module):
             q = XPosFunction.apply(q, 1, N // 2, base, gamma, scale_base)
             k = XPosFunction.apply(k, -1, N // 2, base, gamma, scale_base)
         a = DilatedAttentionFunction.apply(q, k, v, self.patterns, self.causal, None)
-        return _linear(self.out_proj, self.ln_sub(a.reshape(B, N, E)))
+        return _linear(self.out_proj, _layer_norm(self.ln_sub, a.reshape(B, N, E)))
 
     def float64_params(self) -> dict:
         """The parameters as float64 NumPy arrays, keyed ln_in_g, ln_in_b, wq,

@@ -230,3 +230,63 @@ def wgrad(dy: torch.Tensor, x: torch.Tensor, out: torch.Tensor | None = None,
         raise _lib.DilatedAttnError(rc, lib)
     ws.record_stream(stream)
     return out
+
+
+def layer_norm(x: torch.Tensor, weight: torch.Tensor, bias: torch.Tensor, eps: float = 1e-5,
+               stream: torch.cuda.Stream | None = None):
+    """LayerNorm over the last dimension of a contiguous bf16 tensor on the
+    GPU (E a multiple of 8, at most 2048).  Returns (y, mean, rstd), the
+    statistics float32 per row for layer_norm_bwd."""
+    lib = _lib.load()
+    if x.device.type != "cuda":
+        raise RuntimeError("layer_norm runs on the GPU only; x must be a device tensor")
+    if not x.is_contiguous() or not weight.is_contiguous() or not bias.is_contiguous():
+        raise ValueError("x, weight and bias must be contiguous")
+    E = x.shape[-1]
+    if weight.shape != (E,) or bias.shape != (E,) or weight.dtype != x.dtype or bias.dtype != x.dtype:
+        raise ValueError("weight and bias must be [E] tensors of x's dtype")
+    rows = x.numel() // E
+    y = torch.empty_like(x)
+    mean = torch.empty(x.shape[:-1], dtype=torch.float32, device=x.device)
+    rstd = torch.empty_like(mean)
+    if stream is None:
+        stream = torch.cuda.current_stream(x.device)
+    rc = lib.dilated_attn_layernorm_fwd(x.data_ptr(), weight.data_ptr(), bias.data_ptr(), y.data_ptr(),
+                                        mean.data_ptr(), rstd.data_ptr(), rows, E, float(eps),
+                                        _dtype_code(x.dtype), stream.cuda_stream)
+    if rc != 0:
+        raise _lib.DilatedAttnError(rc, lib)
+    return y, mean, rstd
+
+
+def layer_norm_bwd(dy: torch.Tensor, x: torch.Tensor, weight: torch.Tensor, mean: torch.Tensor,
+                   rstd: torch.Tensor, stream: torch.cuda.Stream | None = None):
+    """Gradients (dx, dweight, dbias) of layer_norm given its saved mean and
+    rstd; the float32 workspace comes from torch's caching allocator."""
+    lib = _lib.load()
+    if dy.device.type != "cuda" or x.device != dy.device:
+        raise RuntimeError("layer_norm_bwd runs on the GPU only")
+    if dy.shape != x.shape or dy.dtype != x.dtype or not dy.is_contiguous() or not x.is_contiguous():
+        raise ValueError("dy and x must be contiguous tensors of one shape and dtype")
+    E = x.shape[-1]
+    rows = x.numel() // E
+    if mean.numel() != rows or rstd.numel() != rows or mean.dtype != torch.float32 or rstd.dtype != torch.float32 \
+            or not mean.is_contiguous() or not rstd.is_contiguous() or not weight.is_contiguous():
+        raise ValueError("mean and rstd must be contiguous float32 tensors of one value per row")
+    need = ctypes.c_uint64(0)
+    rc = lib.dilated_attn_layernorm_bwd_workspace(rows, E, ctypes.byref(need))
+    if rc != 0:
+        raise _lib.DilatedAttnError(rc, lib)
+    dx = torch.empty_like(x)
+    dw = torch.empty((E,), dtype=x.dtype, device=x.device)
+    db = torch.empty_like(dw)
+    ws = torch.empty(max(need.value, 16), dtype=torch.uint8, device=x.device)
+    if stream is None:
+        stream = torch.cuda.current_stream(x.device)
+    rc = lib.dilated_attn_layernorm_bwd(dy.data_ptr(), x.data_ptr(), weight.data_ptr(), mean.data_ptr(),
+                                        rstd.data_ptr(), dx.data_ptr(), dw.data_ptr(), db.data_ptr(), rows, E,
+                                        _dtype_code(x.dtype), ws.data_ptr(), need.value, stream.cuda_stream)
+    if rc != 0:
+        raise _lib.DilatedAttnError(rc, lib)
+    ws.record_stream(stream)
+    return dx, dw, db

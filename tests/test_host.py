@@ -52,7 +52,9 @@ def test_exports_every_declared_symbol(lib):
     assert set(names) == {"dilated_attn_plan", "dilated_attn_fwd", "dilated_attn_strerror",
                           "dilated_attn_profile_begin", "dilated_attn_profile_end",
                           "dilated_attn_bwd_plan", "dilated_attn_bwd", "dilated_attn_xpos",
-                          "dilated_attn_wgrad_workspace", "dilated_attn_wgrad"}
+                          "dilated_attn_wgrad_workspace", "dilated_attn_wgrad",
+                          "dilated_attn_layernorm_fwd", "dilated_attn_layernorm_bwd_workspace",
+                          "dilated_attn_layernorm_bwd"}
     for n in names:
         assert hasattr(lib, n), n
     nm = subprocess.run(["nm", "-D", "--defined-only", os.path.join(ROOT, "paper_2307_02486_amd",
@@ -283,3 +285,37 @@ def test_wgrad_rejects_bad_arguments(lib, args, code):
     dy at 256, x at 512 and dw at 1 << 24 (sizes small enough not to meet)."""
     K, M, N, dtype, ws, wsb = args
     assert lib.dilated_attn_wgrad(256, 512, 1 << 24, K, M, N, dtype, ws, wsb, None) == code
+
+
+@pytest.mark.parametrize("args,code", [
+    # (x, g, b, y, mean, rstd, rows, E, eps, dtype)
+    ((256, 1 << 20, 1 << 21, 1 << 22, 1 << 23, 1 << 24, 4, 12, 1e-5, 1), -1),      # E not a multiple of 8
+    ((256, 1 << 20, 1 << 21, 1 << 22, 1 << 23, 1 << 24, 4, 2056, 1e-5, 1), -1),    # E above 2048
+    ((256, 1 << 20, 1 << 21, 1 << 22, 1 << 23, 1 << 24, 4, 64, 0.0, 1), -1),       # eps 0
+    ((256, 1 << 20, 1 << 21, 1 << 22, 1 << 23, 1 << 24, 4, 64, 1e-5, 0), -2),      # float32: no kernel
+    ((264, 1 << 20, 1 << 21, 1 << 22, 1 << 23, 1 << 24, 4, 64, 1e-5, 1), -4),      # x misaligned
+    ((256, 1 << 20, 1 << 21, 512, 1 << 23, 1 << 24, 4, 64, 1e-5, 1), -1),          # y overlaps x
+    ((256, 1 << 20, 1 << 21, 1 << 22, 1 << 22, 1 << 24, 4, 64, 1e-5, 1), -1),      # mean overlaps y
+    ((256, 1 << 20, 1 << 21, 1 << 22, 1 << 23, 1 << 24, -1, 64, 1e-5, 1), -1),     # negative rows
+])
+def test_layernorm_fwd_rejects_bad_arguments(lib, args, code):
+    """Argument checks come before any launch: dummy pointers are never used."""
+    assert lib.dilated_attn_layernorm_fwd(*args, None) == code
+
+
+def test_layernorm_bwd_workspace_and_errors(lib):
+    import ctypes
+    out = ctypes.c_uint64(0)
+    assert lib.dilated_attn_layernorm_bwd_workspace(32768, 768, ctypes.byref(out)) == 0
+    assert out.value == (512 + 16) * 2 * 768 * 4          # 512 workgroups of 64 rows, 16 slices of 32
+    assert lib.dilated_attn_layernorm_bwd_workspace(0, 768, ctypes.byref(out)) == 0 and out.value == 0
+    assert lib.dilated_attn_layernorm_bwd_workspace(64, 20, ctypes.byref(out)) == -1
+    # dy, x, g, mean, rstd, dx, dg, db at disjoint dummy addresses; rows 4, E 64
+    ptrs = [1 << 20, 1 << 21, 1 << 22, 1 << 23, 1 << 24, 1 << 25, 1 << 26, 1 << 27]
+    ws = 1 << 28
+    call = lambda p, w=ws, wb=1 << 20, dtype=1: lib.dilated_attn_layernorm_bwd(*p, 4, 64, dtype, w, wb, None)  # noqa: E731
+    assert call(ptrs, wb=16) == -3                                      # workspace too small
+    assert call(ptrs, dtype=0) == -2
+    assert call(ptrs[:5] + [ptrs[0]] + ptrs[6:]) == -1                  # dx aliases dy
+    assert call(ptrs, w=ptrs[6]) == -1                                  # workspace aliases dg
+    assert call(ptrs, w=None) == -1
