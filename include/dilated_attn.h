@@ -293,7 +293,7 @@ int dilated_attn_layernorm_fwd(const void* x, const void* g, const void* b, void
  *             unspecified.
  * stream      a hipStream_t (NULL = the default stream); asynchronous.
  *
- * Float32 arithmetic; dg and db summed per 64 rows and then over those sums
+ * Float32 arithmetic; dg and db summed per 32 rows and then over those sums
  * in a fixed order (the result does not depend on scheduling), rounded to
  * bf16 once.  Outputs and workspace must not overlap each other or any
  * input.  Returns DA_OK or a negative code; errors launch nothing.

@@ -5,12 +5,13 @@
 // Forward: one wave per row; each lane holds J chunks of 8 elements
 // (chunk c = lane + 64 j), the mean and then the variance of the deviations
 // come from two wave sums, y = (x - mean) rstd g + b.
-// Backward: one wave per row as well, 16 rows per wave and 64 per workgroup;
+// Backward: one wave per row as well, 8 rows per wave and 32 per workgroup;
 // with xhat = (x - mean) rstd recomputed from the saved statistics and
 // dxhat = dy g,  dx = rstd (dxhat - mean(dxhat) - xhat mean(dxhat xhat)).
 // The parameter gradients dg = sum_rows dy xhat and db = sum_rows dy are
-// summed per lane over a wave's rows, per workgroup in LDS, and then over
-// workgroups by two small reduction kernels (deterministic order).
+// summed per lane over a wave's rows, over the workgroup's waves through LDS,
+// and then over workgroups by two small reduction kernels, all in a fixed
+// order (the result does not depend on scheduling).
 #include <hip/hip_runtime.h>
 
 #include "device_common.h"
@@ -19,7 +20,7 @@ namespace da {
 namespace {
 
 constexpr int kLnThreads = 256;
-constexpr int kLnRowsPerWave = 16;
+constexpr int kLnRowsPerWave = 8;
 constexpr int kLnRowsPerWg = kLnRowsPerWave * kLnThreads / 64;
 constexpr int kLnSlice = 32;  // workgroup partials summed per thread in the first reduction
 
@@ -29,14 +30,15 @@ __device__ inline float wave_sum(float v) {
   return v;
 }
 
-__device__ inline void load8f(const u16* p, float* f) {
-  const u32x4 w = *reinterpret_cast<const u32x4*>(p);
+__device__ inline void unpack8(const u32x4 w, float* f) {
 #pragma unroll
   for (int i = 0; i < 4; ++i) {
     f[2 * i] = __builtin_bit_cast(float, w[i] << 16);
     f[2 * i + 1] = __builtin_bit_cast(float, w[i] & 0xffff0000u);
   }
 }
+
+__device__ inline void load8f(const u16* p, float* f) { unpack8(*reinterpret_cast<const u32x4*>(p), f); }
 
 __device__ inline void store8bf(u16* p, const float* f) {
   u32x4 w;
@@ -116,11 +118,10 @@ struct LnBwdArgs {
 
 template <int J>
 __global__ __launch_bounds__(kLnThreads) void ln_bwd(LnBwdArgs a) {
-  __shared__ float red[2 * 2048];
+  extern __shared__ __attribute__((aligned(16))) float red[];  // [4 waves][2E]
   const int tid = __builtin_amdgcn_workitem_id_x();
   const int lane = tid & 63, wv = tid >> 6;
   const int nch = a.E >> 3;
-  for (int i = tid; i < 2 * a.E; i += kLnThreads) red[i] = 0.0f;
   float g[J][8], pg[J][8], pb[J][8];
 #pragma unroll
   for (int j = 0; j < J; ++j) {
@@ -131,26 +132,43 @@ __global__ __launch_bounds__(kLnThreads) void ln_bwd(LnBwdArgs a) {
   }
   const float inv_e = 1.0f / static_cast<float>(a.E);
   const int64_t r0 = static_cast<int64_t>(__builtin_amdgcn_workgroup_id_x()) * kLnRowsPerWg + wv * kLnRowsPerWave;
-  for (int i = 0; i < kLnRowsPerWave; ++i) {
-    const int64_t row = r0 + i;
-    if (row >= a.rows) break;  // wave-uniform
-    const float mean = a.mean[row], rstd = a.rstd[row];
-    float xh[J][8], dxh[J][8];
-    float s1 = 0.0f, s2 = 0.0f;
+  const int nrow = static_cast<int>(min(static_cast<int64_t>(kLnRowsPerWave), a.rows - r0));  // may be <= 0
+  // Row i + 1's x and dy are loaded (as raw bf16) while row i is processed.
+  u32x4 nx[J], ndy[J];
+  auto load_row = [&](int64_t row) {
 #pragma unroll
     for (int j = 0; j < J; ++j) {
       const int c = lane + 64 * j;
       if (c < nch) {
+        nx[j] = *reinterpret_cast<const u32x4*>(a.x + row * a.E + 8 * c);
+        ndy[j] = *reinterpret_cast<const u32x4*>(a.dy + row * a.E + 8 * c);
+      }
+    }
+  };
+  if (nrow > 0) load_row(r0);
+  for (int i = 0; i < nrow; ++i) {
+    const int64_t row = r0 + i;
+    const float mean = a.mean[row], rstd = a.rstd[row];
+    u32x4 xr[J], dyr[J];
+#pragma unroll
+    for (int j = 0; j < J; ++j) {
+      xr[j] = nx[j];
+      dyr[j] = ndy[j];
+    }
+    if (i + 1 < nrow) load_row(row + 1);
+    float s1 = 0.0f, s2 = 0.0f;
+#pragma unroll
+    for (int j = 0; j < J; ++j) {
+      if (lane + 64 * j < nch) {
         float x[8], dy[8];
-        load8f(a.x + row * a.E + 8 * c, x);
-        load8f(a.dy + row * a.E + 8 * c, dy);
+        unpack8(xr[j], x);
+        unpack8(dyr[j], dy);
 #pragma unroll
         for (int e = 0; e < 8; ++e) {
-          xh[j][e] = (x[e] - mean) * rstd;
-          dxh[j][e] = dy[e] * g[j][e];
-          s1 += dxh[j][e];
-          s2 += dxh[j][e] * xh[j][e];
-          pg[j][e] += dy[e] * xh[j][e];
+          const float xh = (x[e] - mean) * rstd, dxh = dy[e] * g[j][e];
+          s1 += dxh;
+          s2 += dxh * xh;
+          pg[j][e] += dy[e] * xh;
           pb[j][e] += dy[e];
         }
       }
@@ -160,27 +178,30 @@ __global__ __launch_bounds__(kLnThreads) void ln_bwd(LnBwdArgs a) {
     for (int j = 0; j < J; ++j) {
       const int c = lane + 64 * j;
       if (c < nch) {
-        float dx[8];
+        float x[8], dy[8], dx[8];
+        unpack8(xr[j], x);
+        unpack8(dyr[j], dy);
 #pragma unroll
-        for (int e = 0; e < 8; ++e) dx[e] = rstd * (dxh[j][e] - m1 - xh[j][e] * m2);
+        for (int e = 0; e < 8; ++e) dx[e] = rstd * (dy[e] * g[j][e] - m1 - (x[e] - mean) * rstd * m2);
         store8bf(a.dx + row * a.E + 8 * c, dx);
       }
     }
   }
-  __syncthreads();
+  float* mine = red + wv * 2 * a.E;
 #pragma unroll
   for (int j = 0; j < J; ++j) {
     const int c = lane + 64 * j;
-    if (c < nch)
-#pragma unroll
-      for (int e = 0; e < 8; ++e) {
-        atomicAdd(&red[8 * c + e], pg[j][e]);
-        atomicAdd(&red[a.E + 8 * c + e], pb[j][e]);
-      }
+    if (c < nch) {
+      *reinterpret_cast<f32x4*>(mine + 8 * c) = f32x4{pg[j][0], pg[j][1], pg[j][2], pg[j][3]};
+      *reinterpret_cast<f32x4*>(mine + 8 * c + 4) = f32x4{pg[j][4], pg[j][5], pg[j][6], pg[j][7]};
+      *reinterpret_cast<f32x4*>(mine + a.E + 8 * c) = f32x4{pb[j][0], pb[j][1], pb[j][2], pb[j][3]};
+      *reinterpret_cast<f32x4*>(mine + a.E + 8 * c + 4) = f32x4{pb[j][4], pb[j][5], pb[j][6], pb[j][7]};
+    }
   }
   __syncthreads();
   float* out = a.part + static_cast<int64_t>(__builtin_amdgcn_workgroup_id_x()) * 2 * a.E;
-  for (int i = tid; i < 2 * a.E; i += kLnThreads) out[i] = red[i];
+  for (int i = tid; i < 2 * a.E; i += kLnThreads)
+    out[i] = (red[i] + red[2 * a.E + i]) + (red[4 * a.E + i] + red[6 * a.E + i]);
 }
 
 // part [nwg][W] -> part2 [ceil(nwg / kLnSlice)][W]: column sums over slices of kLnSlice rows.
@@ -190,6 +211,7 @@ __global__ __launch_bounds__(kLnThreads) void ln_reduce_slices(const float* part
   if (col >= W) return;
   const int r1 = min(nwg, (sl + 1) * kLnSlice);
   float s = 0.0f;
+#pragma unroll 8
   for (int r = sl * kLnSlice; r < r1; ++r) s += part[static_cast<int64_t>(r) * W + col];
   part2[static_cast<int64_t>(sl) * W + col] = s;
 }
@@ -199,6 +221,7 @@ __global__ __launch_bounds__(kLnThreads) void ln_reduce_final(const float* part2
   const int col = __builtin_amdgcn_workgroup_id_x() * kLnThreads + __builtin_amdgcn_workitem_id_x();
   if (col >= 2 * E) return;
   float s = 0.0f;
+#pragma unroll 8
   for (int r = 0; r < S; ++r) s += part2[static_cast<int64_t>(r) * 2 * E + col];
   u16* dst = col < E ? dg + col : db + (col - E);
   *dst = __builtin_bit_cast(u16, (__bf16)s);
@@ -237,10 +260,11 @@ hipError_t launch_layernorm_bwd(const void* dy, const void* x, const void* g, co
   const int J = static_cast<int>((E / 8 + 63) / 64);
   const dim3 grid(static_cast<unsigned>(nwg));
   const int W = static_cast<int>(2 * E);
+  const size_t smem = static_cast<size_t>(kLnThreads / 64) * 2 * E * sizeof(float);
   if (nwg > 0) {  // no rows: only the final kernel, which then writes zeros
-    if (J == 1) hipLaunchKernelGGL(ln_bwd<1>, grid, dim3(kLnThreads), 0, stream, a);
-    else if (J == 2) hipLaunchKernelGGL(ln_bwd<2>, grid, dim3(kLnThreads), 0, stream, a);
-    else hipLaunchKernelGGL(ln_bwd<4>, grid, dim3(kLnThreads), 0, stream, a);
+    if (J == 1) hipLaunchKernelGGL(ln_bwd<1>, grid, dim3(kLnThreads), smem, stream, a);
+    else if (J == 2) hipLaunchKernelGGL(ln_bwd<2>, grid, dim3(kLnThreads), smem, stream, a);
+    else hipLaunchKernelGGL(ln_bwd<4>, grid, dim3(kLnThreads), smem, stream, a);
     hipLaunchKernelGGL(ln_reduce_slices, dim3(static_cast<unsigned>((W + kLnThreads - 1) / kLnThreads),
                                             static_cast<unsigned>(S)),
                        dim3(kLnThreads), 0, stream, part, part2, static_cast<int>(nwg), W);

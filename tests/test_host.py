@@ -307,7 +307,7 @@ def test_layernorm_bwd_workspace_and_errors(lib):
     import ctypes
     out = ctypes.c_uint64(0)
     assert lib.dilated_attn_layernorm_bwd_workspace(32768, 768, ctypes.byref(out)) == 0
-    assert out.value == (512 + 16) * 2 * 768 * 4          # 512 workgroups of 64 rows, 16 slices of 32
+    assert out.value == (1024 + 32) * 2 * 768 * 4         # 1024 workgroups of 32 rows, 32 slices of 32
     assert lib.dilated_attn_layernorm_bwd_workspace(0, 768, ctypes.byref(out)) == 0 and out.value == 0
     assert lib.dilated_attn_layernorm_bwd_workspace(64, 20, ctypes.byref(out)) == -1
     # dy, x, g, mean, rstd, dx, dg, db at disjoint dummy addresses; rows 4, E 64
