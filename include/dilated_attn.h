@@ -202,7 +202,7 @@ int dilated_attn_bwd(const void* q, const void* k, const void* v, const void* ou
  *
  * x, y        device pointers, [B, N, H, D] of dtype, 16-byte aligned; y may
  *             equal x (in place) but must not overlap it otherwise.
- * D           a multiple of 8, 8 <= D <= 256.
+ * D           a multiple of 8, 8 <= D <= 256; B * N * H * D <= 2^34.
  * center      in [0, N).
  * base > 1, gamma > 0, scale_base > 0, all finite.  The scale exponents
  *             |n - center| / scale_base * |log2 zeta_i| must stay <= 64 for
@@ -260,7 +260,7 @@ int dilated_attn_wgrad(const void* dy, const void* x, void* dw, int64_t K, int64
  *             NULL when rows = 0.
  * g, b        device pointers, [E] bf16, 16-byte aligned.
  * mean, rstd  device pointers, [rows] float32 (outputs, kept for the backward).
- * rows        0 <= rows <= 2^31.
+ * rows        0 <= rows <= 2^26.
  * E           a multiple of 8, 8 <= E <= 2048.
  * eps         finite, > 0.
  * dtype       DA_BF16 (others: DA_EUNSUPPORTED).

@@ -178,8 +178,9 @@ int dilated_attn_xpos(const void* x, void* y, int64_t B, int64_t N, int64_t H, i
   if (!std::isfinite(base) || !(base > 1.0f) || !std::isfinite(gamma) || !(gamma > 0.0f) ||
       !std::isfinite(scale_base) || !(scale_base > 0.0f))
     return DA_EINVAL;
-  if (B > (int64_t{1} << 40) / N || B * N > (int64_t{1} << 40) / H ||
-      B * N * H > (int64_t{1} << 40) / D)
+  // At most 2^34 elements: one thread per 8 keeps the grid within 2^32 work-items.
+  if (B > (int64_t{1} << 34) / N || B * N > (int64_t{1} << 34) / H ||
+      B * N * H > (int64_t{1} << 34) / D)
     return DA_EINVAL;
   // zeta_i ranges over [gamma / (1 + gamma), 1): the smallest gives the
   // largest |log2 zeta| (every zeta_i < 1 for gamma > 0 and i < D/2).
@@ -228,7 +229,7 @@ int dilated_attn_wgrad(const void* dy, const void* x, void* dw, int64_t K, int64
 int dilated_attn_layernorm_fwd(const void* x, const void* g, const void* b, void* y, float* mean, float* rstd,
                                int64_t rows, int64_t E, float eps, int64_t dtype, void* stream) {
   if (!g || !b || !y || !mean || !rstd || (rows > 0 && !x)) return DA_EINVAL;
-  if (rows < 0 || rows > (int64_t{1} << 31) || E < 8 || E > 2048 || E % 8 || !std::isfinite(eps) || !(eps > 0.0f))
+  if (rows < 0 || rows > (int64_t{1} << 26) || E < 8 || E > 2048 || E % 8 || !std::isfinite(eps) || !(eps > 0.0f))
     return DA_EINVAL;
   if (dtype != DA_BF16) return DA_EUNSUPPORTED;
   if (!aligned16(x) || !aligned16(g) || !aligned16(b) || !aligned16(y)) return DA_EALIGN;
@@ -251,7 +252,7 @@ int dilated_attn_layernorm_fwd(const void* x, const void* g, const void* b, void
 }
 
 int dilated_attn_layernorm_bwd_workspace(int64_t rows, int64_t E, uint64_t* bytes) {
-  if (!bytes || rows < 0 || rows > (int64_t{1} << 31) || E < 8 || E > 2048 || E % 8) return DA_EINVAL;
+  if (!bytes || rows < 0 || rows > (int64_t{1} << 26) || E < 8 || E > 2048 || E % 8) return DA_EINVAL;
   *bytes = da::layernorm_bwd_workspace(rows, E);
   return DA_OK;
 }

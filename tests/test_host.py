@@ -246,6 +246,7 @@ def test_bwd_unsupported_and_errors(lib):
     ((1, 40000, 1, 64, 1, 0, 20000, 1e4, 0.4, 512.0, 1), -1),  # scale exponents beyond 64
     ((1, 16, 2, 64, 1, 0, 8, 1e4, 0.4, 512.0, 7), -2),      # unknown dtype
     ((0, 16, 2, 64, 1, 0, 8, 1e4, 0.4, 512.0, 1), -1),
+    ((2, 1 << 30, 2, 8, 1, 0, 8, 1e4, 0.4, 512.0, 1), -1),  # 2^35 elements: beyond a 32-bit grid
 ])
 def test_xpos_rejects_bad_arguments(lib, args, code):
     """Argument checks come before any launch: dummy pointers are never used."""
@@ -297,6 +298,7 @@ def test_wgrad_rejects_bad_arguments(lib, args, code):
     ((256, 1 << 20, 1 << 21, 512, 1 << 23, 1 << 24, 4, 64, 1e-5, 1), -1),          # y overlaps x
     ((256, 1 << 20, 1 << 21, 1 << 22, 1 << 22, 1 << 24, 4, 64, 1e-5, 1), -1),      # mean overlaps y
     ((256, 1 << 20, 1 << 21, 1 << 22, 1 << 23, 1 << 24, -1, 64, 1e-5, 1), -1),     # negative rows
+    ((256, 1 << 20, 1 << 21, 1 << 22, 1 << 23, 1 << 24, (1 << 26) + 1, 8, 1e-5, 1), -1),  # beyond 2^26 rows
 ])
 def test_layernorm_fwd_rejects_bad_arguments(lib, args, code):
     """Argument checks come before any launch: dummy pointers are never used."""
