@@ -219,18 +219,20 @@ int dilated_attn_xpos(const void* x, void* y, int64_t B, int64_t N, int64_t H, i
                       float scale_base, int64_t dtype, void* stream);
 
 /*
- * dilated_attn_wgrad - weight gradient of a linear projection of the layer
- * around the dilated attention (the Q, K, V and output projections of the
- * paper's Magneto-based language model, Sec. 4.1):
- *   dw[m][n] = sum over k < K of dy[k][m] * x[k][n]
- * for a projection y = x w^T (+ bias) applied to K = B * N rows, dy its
- * incoming gradient.  The long reduction over rows is split into chunks
- * whose float32 partial sums go to the workspace and are then added.
+ * dilated_attn_wgrad - weight (and bias) gradient of a linear projection of
+ * the layer around the dilated attention (the Q, K, V and output projections
+ * of the paper's Magneto-based language model, Sec. 4.1):
+ *   dw[m][n] = sum over k < K of dy[k][m] * x[k][n],   db[m] = sum over k of dy[k][m]
+ * for a projection y = x w^T + b applied to K = B * N rows, dy its incoming
+ * gradient.  The long reduction over rows is split into chunks whose float32
+ * partial sums go to the workspace and are then added.
  *
  * dy          device pointer, [K, M] bf16 row-major (may be NULL when K = 0).
  * x           device pointer, [K, N] bf16 row-major (may be NULL when K = 0).
  * dw          device pointer, [M, N] bf16 row-major (output, overwritten;
- *             all zeros when K = 0).  Must not overlap dy, x or workspace.
+ *             all zeros when K = 0).
+ * db          device pointer, [M] bf16 (output), or NULL for no bias gradient.
+ *             dw, db and workspace must not overlap each other, dy or x.
  * K           0 <= K <= 2^30.
  * M, N        multiples of 128, at most 16384.
  * dtype       DA_BF16 (others: DA_EUNSUPPORTED).
@@ -240,13 +242,15 @@ int dilated_attn_xpos(const void* x, void* y, int64_t B, int64_t N, int64_t H, i
  *             ignored, on return unspecified.
  * stream      a hipStream_t (NULL = the default stream); asynchronous.
  *
- * Products and sums in float32 (matrix cores), dw rounded to bf16 once.
+ * Products and sums in float32 (matrix cores; db on the vector units, summed
+ * per 256-row slice and then over the slices), rounded to bf16 once.
  * All device pointers 16-byte aligned.  Returns DA_OK or a negative code;
  * errors launch nothing.
  */
 int dilated_attn_wgrad_workspace(int64_t K, int64_t M, int64_t N, uint64_t* bytes);
-int dilated_attn_wgrad(const void* dy, const void* x, void* dw, int64_t K, int64_t M, int64_t N,
-                       int64_t dtype, void* workspace, uint64_t workspace_bytes, void* stream);
+int dilated_attn_wgrad(const void* dy, const void* x, void* dw, void* db, int64_t K, int64_t M,
+                       int64_t N, int64_t dtype, void* workspace, uint64_t workspace_bytes,
+                       void* stream);
 
 /*
  * dilated_attn_layernorm_fwd - LayerNorm of the layer around the dilated

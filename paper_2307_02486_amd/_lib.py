@@ -72,7 +72,7 @@ def load():
     lib.dilated_attn_xpos.restype = ctypes.c_int
     lib.dilated_attn_wgrad_workspace.argtypes = [i64, i64, i64, ctypes.POINTER(ctypes.c_uint64)]
     lib.dilated_attn_wgrad_workspace.restype = ctypes.c_int
-    lib.dilated_attn_wgrad.argtypes = [vp, vp, vp, i64, i64, i64, i64, vp, ctypes.c_uint64, vp]
+    lib.dilated_attn_wgrad.argtypes = [vp, vp, vp, vp, i64, i64, i64, i64, vp, ctypes.c_uint64, vp]
     lib.dilated_attn_wgrad.restype = ctypes.c_int
     lib.dilated_attn_layernorm_fwd.argtypes = [vp, vp, vp, vp, vp, vp, i64, i64, f32, i64, vp]
     lib.dilated_attn_layernorm_fwd.restype = ctypes.c_int

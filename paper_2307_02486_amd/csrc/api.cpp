@@ -200,28 +200,31 @@ int dilated_attn_wgrad_workspace(int64_t K, int64_t M, int64_t N, uint64_t* byte
   if (!bytes) return DA_EINVAL;
   if (K < 0 || K > (int64_t{1} << 30) || M <= 0 || N <= 0 || M % 128 || N % 128 || M > 16384 || N > 16384)
     return DA_EINVAL;
-  int64_t chunk = 0;
-  *bytes = static_cast<uint64_t>(da::wgrad_splits(K, M, N, &chunk)) * M * N * 4;
+  *bytes = da::wgrad_workspace(K, M, N);
   return DA_OK;
 }
 
-int dilated_attn_wgrad(const void* dy, const void* x, void* dw, int64_t K, int64_t M, int64_t N,
+int dilated_attn_wgrad(const void* dy, const void* x, void* dw, void* db, int64_t K, int64_t M, int64_t N,
                        int64_t dtype, void* workspace, uint64_t workspace_bytes, void* stream) {
   uint64_t need = 0;
   if (!dw || (K > 0 && (!dy || !x))) return DA_EINVAL;
   if (dilated_attn_wgrad_workspace(K, M, N, &need) != DA_OK) return DA_EINVAL;
   if (dtype != DA_BF16) return DA_EUNSUPPORTED;
   if (need > 0 && !workspace) return DA_EINVAL;
-  if (!aligned16(dy) || !aligned16(x) || !aligned16(dw) || (need > 0 && !aligned16(workspace)))
+  if (!aligned16(dy) || !aligned16(x) || !aligned16(dw) || !aligned16(db) || (need > 0 && !aligned16(workspace)))
     return DA_EALIGN;
   if (workspace_bytes < need) return DA_EWORKSPACE;
-  const uint64_t dwb = static_cast<uint64_t>(M * N) * 2;
-  if (overlaps(dw, dwb, dy, static_cast<uint64_t>(K * M) * 2) || overlaps(dw, dwb, x, static_cast<uint64_t>(K * N) * 2))
-    return DA_EINVAL;
-  if (need > 0 && (overlaps(workspace, need, dw, dwb) || overlaps(workspace, need, dy, static_cast<uint64_t>(K * M) * 2) ||
-                   overlaps(workspace, need, x, static_cast<uint64_t>(K * N) * 2)))
-    return DA_EINVAL;
-  if (da::launch_wgrad(dy, x, dw, K, M, N, workspace, static_cast<hipStream_t>(stream)) != hipSuccess)
+  const void* ins[2] = {dy, x};
+  const uint64_t isz[2] = {static_cast<uint64_t>(K * M) * 2, static_cast<uint64_t>(K * N) * 2};
+  const void* outs[3] = {dw, db, workspace};
+  const uint64_t osz[3] = {static_cast<uint64_t>(M * N) * 2, db ? static_cast<uint64_t>(M) * 2 : 0, need};
+  for (int i = 0; i < 3; ++i) {
+    for (int j = i + 1; j < 3; ++j)
+      if (overlaps(outs[i], osz[i], outs[j], osz[j])) return DA_EINVAL;
+    for (int j = 0; j < 2; ++j)
+      if (overlaps(outs[i], osz[i], ins[j], isz[j])) return DA_EINVAL;
+  }
+  if (da::launch_wgrad(dy, x, dw, db, K, M, N, workspace, static_cast<hipStream_t>(stream)) != hipSuccess)
     return DA_EHIP;
   return DA_OK;
 }

@@ -63,9 +63,11 @@ hipError_t launch_xpos(const void* x, void* y, int64_t B, int64_t N, int64_t H, 
 
 // Weight gradient dw[M][N] = sum_k dy[k][M] x[k][N] (bf16, M and N multiples
 // of 128): float32 partial sums over k-chunks in workspace, then their sum.
+// With db non-null, also db[M] = the column sums of dy (the bias gradient).
 int64_t wgrad_splits(int64_t K, int64_t M, int64_t N, int64_t* chunk);
-hipError_t launch_wgrad(const void* dy, const void* x, void* dw, int64_t K, int64_t M, int64_t N, void* workspace,
-                        hipStream_t stream);
+uint64_t wgrad_workspace(int64_t K, int64_t M, int64_t N);
+hipError_t launch_wgrad(const void* dy, const void* x, void* dw, void* db, int64_t K, int64_t M, int64_t N,
+                        void* workspace, hipStream_t stream);
 
 // LayerNorm over rows of E bf16 elements (E a multiple of 8, at most 2048),
 // float32 statistics; the backward's parameter gradients go through a

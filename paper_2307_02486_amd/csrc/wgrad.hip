@@ -171,7 +171,85 @@ __global__ __launch_bounds__(kWgThreads) void wgrad_sum(const float* part, u16* 
                                             o[2] | (static_cast<unsigned>(o[3]) << 16)};
 }
 
+// Bias gradient db[m] = sum_k dy[k][m], in two steps.  colsum_partial: the
+// workgroup (column block bx, slice y) sums rows [y rs, (y + 1) rs) of 512
+// columns, each lane 8 columns (one 16-byte load per row) over every fourth
+// row, the four row lanes combined through LDS, into part[y][M].
+__global__ __launch_bounds__(kWgThreads) void colsum_partial(const u16* dy, float* part, int64_t K, int M, int rs,
+                                                             int col_blocks) {
+  __shared__ __attribute__((aligned(16))) float red[4][64 * 8];
+  const int tid = __builtin_amdgcn_workitem_id_x();
+  const int cgl = tid & 63, rl = tid >> 6;
+  const int blk = __builtin_amdgcn_workgroup_id_x();
+  const int y = blk / col_blocks;
+  const int cg = (blk % col_blocks) * 64 + cgl;  // group of 8 columns
+  const int64_t r0 = static_cast<int64_t>(y) * rs;
+  const int64_t r1 = r0 + rs < K ? r0 + rs : K;
+  float s[8];
+#pragma unroll
+  for (int e = 0; e < 8; ++e) s[e] = 0.0f;
+  if (cg < (M >> 3)) {
+#pragma unroll 8
+    for (int64_t r = r0 + rl; r < r1; r += 4) {
+      const u32x4 w = *reinterpret_cast<const u32x4*>(dy + r * M + 8 * cg);
+#pragma unroll
+      for (int i = 0; i < 4; ++i) {
+        s[2 * i] += __builtin_bit_cast(float, w[i] << 16);
+        s[2 * i + 1] += __builtin_bit_cast(float, w[i] & 0xffff0000u);
+      }
+    }
+  }
+  *reinterpret_cast<f32x4*>(&red[rl][8 * cgl]) = f32x4{s[0], s[1], s[2], s[3]};
+  *reinterpret_cast<f32x4*>(&red[rl][8 * cgl + 4]) = f32x4{s[4], s[5], s[6], s[7]};
+  __syncthreads();
+  if (rl == 0 && cg < (M >> 3)) {
+    float* out = part + static_cast<int64_t>(y) * M + 8 * cg;
+#pragma unroll
+    for (int h = 0; h < 2; ++h) {
+      const f32x4 v = (*reinterpret_cast<const f32x4*>(&red[0][8 * cgl + 4 * h]) +
+                       *reinterpret_cast<const f32x4*>(&red[1][8 * cgl + 4 * h])) +
+                      (*reinterpret_cast<const f32x4*>(&red[2][8 * cgl + 4 * h]) +
+                       *reinterpret_cast<const f32x4*>(&red[3][8 * cgl + 4 * h]));
+      *reinterpret_cast<f32x4*>(out + 4 * h) = v;
+    }
+  }
+}
+
+// colsum_final: db[c] = sum over the R slices of part[y][c], 32 columns per
+// workgroup and 8 row lanes per column, combined through LDS; zeros for R = 0.
+__global__ __launch_bounds__(kWgThreads) void colsum_final(const float* part, u16* db, int M, int R) {
+  __shared__ float red[8][32];
+  const int tid = __builtin_amdgcn_workitem_id_x();
+  const int cl = tid & 31, rl = tid >> 5;
+  const int c = __builtin_amdgcn_workgroup_id_x() * 32 + cl;  // M is a multiple of 32
+  float s = 0.0f;
+#pragma unroll 16
+  for (int y = rl; y < R; y += 8) s += part[static_cast<int64_t>(y) * M + c];
+  red[rl][cl] = s;
+  __syncthreads();
+  if (rl == 0) {
+    const float t = ((red[0][cl] + red[1][cl]) + (red[2][cl] + red[3][cl])) +
+                    ((red[4][cl] + red[5][cl]) + (red[6][cl] + red[7][cl]));
+    db[c] = __builtin_bit_cast(u16, (__bf16)t);
+  }
+}
+
 }  // namespace
+
+// Slices of the bias-gradient column sums: 256 rows each, at most 1024.
+int64_t colsum_slices(int64_t K, int64_t* rows_per_slice) {
+  *rows_per_slice = 0;
+  if (K <= 0) return 0;
+  int64_t R = (K + 255) / 256;
+  if (R > 1024) R = 1024;
+  *rows_per_slice = (K + R - 1) / R;
+  return (K + *rows_per_slice - 1) / *rows_per_slice;
+}
+
+uint64_t wgrad_workspace(int64_t K, int64_t M, int64_t N) {
+  int64_t chunk = 0, rs = 0;
+  return (static_cast<uint64_t>(wgrad_splits(K, M, N, &chunk)) * N + colsum_slices(K, &rs)) * M * 4;
+}
 
 // Splits of the reduction: at most 512 workgroups in all (two per compute
 // unit, as 64 KiB of LDS per workgroup allows) unless the output alone has
@@ -187,8 +265,8 @@ int64_t wgrad_splits(int64_t K, int64_t M, int64_t N, int64_t* chunk) {
   return (K + *chunk - 1) / *chunk;
 }
 
-hipError_t launch_wgrad(const void* dy, const void* x, void* dw, int64_t K, int64_t M, int64_t N, void* workspace,
-                        hipStream_t stream) {
+hipError_t launch_wgrad(const void* dy, const void* x, void* dw, void* db, int64_t K, int64_t M, int64_t N,
+                        void* workspace, hipStream_t stream) {
   int64_t chunk = 0;
   const int64_t splits = wgrad_splits(K, M, N, &chunk);
   WgradArgs a;
@@ -209,6 +287,17 @@ hipError_t launch_wgrad(const void* dy, const void* x, void* dw, int64_t K, int6
   hipLaunchKernelGGL(wgrad_sum, dim3(static_cast<unsigned>((mn / 4 + kWgThreads - 1) / kWgThreads)),
                      dim3(kWgThreads), 0, stream, static_cast<const float*>(workspace), static_cast<u16*>(dw), mn,
                      static_cast<int>(splits));
+  if (db) {
+    int64_t rs = 0;
+    const int64_t R = colsum_slices(K, &rs);
+    float* part = static_cast<float*>(workspace) + splits * mn;
+    const int col_blocks = static_cast<int>((M / 8 + 63) / 64);
+    if (R > 0)
+      hipLaunchKernelGGL(colsum_partial, dim3(static_cast<unsigned>(R * col_blocks)), dim3(kWgThreads), 0, stream,
+                         static_cast<const u16*>(dy), part, K, static_cast<int>(M), static_cast<int>(rs), col_blocks);
+    hipLaunchKernelGGL(colsum_final, dim3(static_cast<unsigned>(M / 32)), dim3(kWgThreads), 0, stream,
+                       static_cast<const float*>(part), static_cast<u16*>(db), static_cast<int>(M), static_cast<int>(R));
+  }
   return hipGetLastError();
 }
 

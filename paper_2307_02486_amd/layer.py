@@ -59,9 +59,9 @@ class XPosFunction(torch.autograd.Function):
 
 
 class LinearFunction(torch.autograd.Function):
-    """y = x w^T + b over the last dimension, with dw = dy^T x from the
-    library's weight-gradient kernel when it applies (bf16, both dimensions
-    multiples of 128) and from torch's GEMM otherwise."""
+    """y = x w^T + b over the last dimension, with dw = dy^T x and db (the
+    column sums of dy) from the library's weight-gradient kernels when they
+    apply (bf16, both dimensions multiples of 128) and from torch otherwise."""
 
     @staticmethod
     def forward(ctx, x, w, b):
@@ -75,10 +75,10 @@ class LinearFunction(torch.autograd.Function):
         x2 = x.reshape(-1, x.shape[-1]).contiguous()
         dx = (dy2 @ w).view(x.shape)
         if dy2.dtype == torch.bfloat16 and dy2.shape[1] % 128 == 0 and x2.shape[1] % 128 == 0:
-            dw = wgrad(dy2, x2)
+            dw, db = wgrad(dy2, x2, bias_grad=True)
         else:
-            dw = dy2.t() @ x2
-        return dx, dw, dy2.sum(0)
+            dw, db = dy2.t() @ x2, dy2.sum(0)
+        return dx, dw, db
 
 
 def _linear(mod: torch.nn.Linear, x: torch.Tensor) -> torch.Tensor:

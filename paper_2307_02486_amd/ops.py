@@ -201,10 +201,11 @@ def xpos(x: torch.Tensor, sign: int, transpose: bool = False, center: int | None
     return out
 
 
-def wgrad(dy: torch.Tensor, x: torch.Tensor, out: torch.Tensor | None = None,
-          stream: torch.cuda.Stream | None = None) -> torch.Tensor:
+def wgrad(dy: torch.Tensor, x: torch.Tensor, out: torch.Tensor | None = None, bias_grad: bool = False,
+          stream: torch.cuda.Stream | None = None):
     """dw = dy^T x for bf16 dy [K, M] and x [K, N] on the GPU (M, N multiples
-    of 128): the weight gradient of a projection y = x w^T.  Enqueued on
+    of 128): the weight gradient of a projection y = x w^T + b.  With
+    bias_grad=True returns (dw, db), db = the column sums of dy.  Enqueued on
     `stream`; the float32 workspace comes from torch's caching allocator."""
     lib = _lib.load()
     if dy.device.type != "cuda" or x.device != dy.device:
@@ -224,12 +225,13 @@ def wgrad(dy: torch.Tensor, x: torch.Tensor, out: torch.Tensor | None = None,
     ws = torch.empty(max(need.value, 16), dtype=torch.uint8, device=dy.device)
     if stream is None:
         stream = torch.cuda.current_stream(dy.device)
-    rc = lib.dilated_attn_wgrad(dy.data_ptr(), x.data_ptr(), out.data_ptr(), K, M, N, _dtype_code(dy.dtype),
-                                ws.data_ptr(), need.value, stream.cuda_stream)
+    db = torch.empty((M,), dtype=dy.dtype, device=dy.device) if bias_grad else None
+    rc = lib.dilated_attn_wgrad(dy.data_ptr(), x.data_ptr(), out.data_ptr(), db.data_ptr() if bias_grad else None,
+                                K, M, N, _dtype_code(dy.dtype), ws.data_ptr(), need.value, stream.cuda_stream)
     if rc != 0:
         raise _lib.DilatedAttnError(rc, lib)
     ws.record_stream(stream)
-    return out
+    return (out, db) if bias_grad else out
 
 
 def layer_norm(x: torch.Tensor, weight: torch.Tensor, bias: torch.Tensor, eps: float = 1e-5,

@@ -263,11 +263,12 @@ def test_wgrad_workspace_sizes(lib):
         rc = lib.dilated_attn_wgrad_workspace(K, M, N, ctypes.byref(out))
         return rc if rc else out.value
 
+    # float32 partials of dw per split, then of db per slice of 256 rows (at most 1024 slices)
     assert ws(0, 768, 768) == 0
-    assert ws(1, 768, 768) == 768 * 768 * 4                 # one k tile: one split
-    assert ws(32768, 768, 768) == 14 * 768 * 768 * 4       # 36 tiles x 14 splits = 504 workgroups
-    assert ws(64 * 100, 128, 128) == 100 * 128 * 128 * 4    # 512 splits capped at the 100 k tiles
-    assert ws(1 << 20, 16384, 16384) == 16384 * 16384 * 4   # more tiles than 512: one split
+    assert ws(1, 768, 768) == (768 + 1) * 768 * 4                # one k tile: one split, one slice
+    assert ws(32768, 768, 768) == (14 * 768 + 128) * 768 * 4     # 36 tiles x 14 splits = 504 workgroups
+    assert ws(64 * 100, 128, 128) == (100 * 128 + 25) * 128 * 4  # 512 splits capped at the 100 k tiles
+    assert ws(1 << 20, 16384, 16384) == (16384 + 1024) * 16384 * 4  # more tiles than 512: one split
     for bad in ((-1, 128, 128), (64, 100, 128), (64, 128, 0), (64, 128, 16512), ((1 << 30) + 1, 128, 128)):
         assert ws(*bad) == -1, bad
 
@@ -283,9 +284,16 @@ def test_wgrad_workspace_sizes(lib):
 ])
 def test_wgrad_rejects_bad_arguments(lib, args, code):
     """Argument checks come before any launch: dummy pointers are never used.
-    dy at 256, x at 512 and dw at 1 << 24 (sizes small enough not to meet)."""
+    dy at 256, x at 512, dw at 1 << 24 and db at 1 << 25 (sizes small enough
+    not to meet)."""
     K, M, N, dtype, ws, wsb = args
-    assert lib.dilated_attn_wgrad(256, 512, 1 << 24, K, M, N, dtype, ws, wsb, None) == code
+    assert lib.dilated_attn_wgrad(256, 512, 1 << 24, 1 << 25, K, M, N, dtype, ws, wsb, None) == code
+
+
+def test_wgrad_rejects_overlapping_bias_gradient(lib):
+    assert lib.dilated_attn_wgrad(256, 512, 1 << 24, (1 << 24) + 64, 64, 128, 128, 1, 1 << 26, 1 << 20, None) == -1
+    assert lib.dilated_attn_wgrad(256, 512, 1 << 24, 1 << 25, 64, 128, 128, 1, 1 << 25, 1 << 20, None) == -1
+    assert lib.dilated_attn_wgrad(256, 512, 1 << 24, (1 << 25) + 8, 64, 128, 128, 1, 1 << 26, 1 << 20, None) == -4
 
 
 @pytest.mark.parametrize("args,code", [

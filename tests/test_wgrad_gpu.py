@@ -1,6 +1,7 @@
 """GPU parity of the projections' weight-gradient kernel (dilated_attn_wgrad):
-dw = dy^T x for bf16 dy [K, M] and x [K, N], against a float32 product of the
-same bf16 values on the GPU.
+dw = dy^T x for bf16 dy [K, M] and x [K, N], and the bias gradient db (the
+column sums of dy), against float32 results of the same bf16 values on the
+GPU.
 
 Bar, elementwise and derived from the arithmetic: the kernel rounds its
 float32 sum to bf16 once (unit roundoff 2^-8), and it and the reference sum
@@ -61,6 +62,15 @@ def test_wgrad_matches_float32_product(case):
     wgrad(dy, x, out=out)
     torch.cuda.synchronize()
     assert torch.equal(out, dw)
+    # with the bias gradient: the same dw, and db within the same kind of bar
+    dw2, db = wgrad(dy, x, bias_grad=True)
+    torch.cuda.synchronize()
+    assert torch.equal(dw2, dw)
+    ref = dy.float().sum(0)
+    bound = 2.0 ** -8 * ref.abs() + 2.0 ** -12 * dy.float().abs().sum(0)
+    worst = float(((db.float() - ref).abs() / bound).max())
+    note(f"[wgrad] db err/bound {worst:.3f}")
+    assert worst <= 1.0
 
 
 def test_wgrad_empty_reduction_gives_zeros():
@@ -70,8 +80,9 @@ def test_wgrad_empty_reduction_gives_zeros():
     x = torch.empty((0, 256), dtype=torch.bfloat16, device="cuda")
     out = torch.full((128, 256), 3.0, dtype=torch.bfloat16, device="cuda")
     wgrad(dy, x, out=out)
+    _, db = wgrad(dy, x, bias_grad=True)
     torch.cuda.synchronize()
-    assert (out == 0).all().item()
+    assert (out == 0).all().item() and (db == 0).all().item()
 
 
 def test_wgrad_errors_launch_nothing():
