@@ -244,9 +244,12 @@ def layer_norm(x: torch.Tensor, weight: torch.Tensor, bias: torch.Tensor, eps: f
         raise RuntimeError("layer_norm runs on the GPU only; x must be a device tensor")
     if not x.is_contiguous() or not weight.is_contiguous() or not bias.is_contiguous():
         raise ValueError("x, weight and bias must be contiguous")
+    if x.dim() == 0 or x.shape[-1] == 0:
+        raise ValueError("x must have a non-empty last dimension")
     E = x.shape[-1]
-    if weight.shape != (E,) or bias.shape != (E,) or weight.dtype != x.dtype or bias.dtype != x.dtype:
-        raise ValueError("weight and bias must be [E] tensors of x's dtype")
+    if weight.shape != (E,) or bias.shape != (E,) or weight.dtype != x.dtype or bias.dtype != x.dtype \
+            or weight.device != x.device or bias.device != x.device:
+        raise ValueError("weight and bias must be [E] tensors of x's dtype and device")
     rows = x.numel() // E
     y = torch.empty_like(x)
     mean = torch.empty(x.shape[:-1], dtype=torch.float32, device=x.device)
@@ -270,8 +273,12 @@ def layer_norm_bwd(dy: torch.Tensor, x: torch.Tensor, weight: torch.Tensor, mean
         raise RuntimeError("layer_norm_bwd runs on the GPU only")
     if dy.shape != x.shape or dy.dtype != x.dtype or not dy.is_contiguous() or not x.is_contiguous():
         raise ValueError("dy and x must be contiguous tensors of one shape and dtype")
+    if x.dim() == 0 or x.shape[-1] == 0:
+        raise ValueError("x must have a non-empty last dimension")
     E = x.shape[-1]
     rows = x.numel() // E
+    if weight.shape != (E,) or weight.dtype != x.dtype or weight.device != x.device:
+        raise ValueError("weight must be an [E] tensor of x's dtype and device")
     if mean.numel() != rows or rstd.numel() != rows or mean.dtype != torch.float32 or rstd.dtype != torch.float32 \
             or not mean.is_contiguous() or not rstd.is_contiguous() or not weight.is_contiguous():
         raise ValueError("mean and rstd must be contiguous float32 tensors of one value per row")
