@@ -73,7 +73,9 @@ class LinearFunction(torch.autograd.Function):
         x, w = ctx.saved_tensors
         dy2 = dy.reshape(-1, dy.shape[-1]).contiguous()
         x2 = x.reshape(-1, x.shape[-1]).contiguous()
-        dx = (dy2 @ w).view(x.shape)
+        dx = (dy2 @ w).view(x.shape) if ctx.needs_input_grad[0] else None
+        if not (ctx.needs_input_grad[1] or ctx.needs_input_grad[2]):
+            return dx, None, None
         if dy2.dtype == torch.bfloat16 and dy2.shape[1] % 128 == 0 and x2.shape[1] % 128 == 0:
             dw, db = wgrad(dy2, x2, bias_grad=True)
         else:
