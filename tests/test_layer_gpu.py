@@ -158,3 +158,27 @@ def test_layer_backward_matches_oracle(case):
         rel = float(np.abs(g - ref).max() / max(np.abs(ref).max(), 1e-30))
         note(f"[layer bwd] d{name}: max-abs err / max|ref| = {rel:.3e}")
         assert rel <= 3e-2, f"d{name}: {rel}"
+
+
+def test_layer_backward_computes_only_requested_gradients():
+    """Frozen parameters get no gradient, an input without requires_grad
+    none either, and the input gradient alone equals the one computed with
+    every parameter's."""
+    B, N, H, D, pats, causal = LAYER_CASES[0]
+    note("[layer bwd] requested gradients only")
+    layer, x = _make_layer(B, N, H, D, pats, causal, torch.bfloat16, 14)
+    dy = workloads.make_random((B, N, H * D), torch.bfloat16, 1.0, 15, "cuda", 0)
+    layer(x).backward(dy)                       # x needs no gradient
+    assert x.grad is None and layer.q_proj.weight.grad is not None
+    x.requires_grad_(True)
+    layer.zero_grad(set_to_none=True)
+    layer(x).backward(dy)
+    dx_full = x.grad.clone()
+    layer.zero_grad(set_to_none=True)
+    for p in layer.parameters():
+        p.requires_grad_(False)
+    x.grad = None
+    layer(x).backward(dy)                       # only x needs a gradient
+    torch.cuda.synchronize()
+    assert all(p.grad is None for p in layer.parameters())
+    assert torch.equal(x.grad, dx_full)
