@@ -9,14 +9,15 @@ Prints one JSON line: effective TFLOP/s over the exact sparse flops (4*D per
 unmasked query-key pair) and tokens/s of the timed back-to-back steps, the
 times of the call's two launches from a second pass in which the library
 records HIP events around them on the call's stream, the attention kernel's
-MFMA roofline fraction and the combine kernel's HBM bandwidth, the same
-figures for the opt-in path that fuses the combine into the epilogue of the
-r = 1 pattern's attention launch (DILATED_ATTN_FUSE_COMBINE=1), and the CPU
+MFMA roofline fraction and the combine kernel's HBM bandwidth, and the CPU
 oracle timed on a bounded sample on this host.  Every timed region follows at
 least --warmup-seconds of untimed calls.  After the timed region, a further
 pass times each step on its own (median, minimum, mean), once as is and once
 with a 512 MiB buffer written before each step so that the inputs are no
-longer held in the Infinity Cache.
+longer held in the Infinity Cache.  Then the same call is timed on the
+N=262144 (H=16, D=64, 8 patterns) and N=1048576 (H=16, D=128, 6 patterns)
+workloads, whose per-pattern workspaces (2.2 and 8.7 GB) are far larger than
+the 256 MB Infinity Cache: their combine launch gives the combine's HBM rate.
 """
 from __future__ import annotations
 
@@ -50,6 +51,9 @@ def parse():
                     help="minimum CPU time spent on the oracle sample (0 skips the CPU baseline)")
     ap.add_argument("--dist-steps", type=int, default=20,
                     help="steps of the per-step pass (unflushed and flushed each); 0 skips it")
+    ap.add_argument("--large", default="n256k_h16_d64_8pat_geo,n1m_h16_d128_6pat",
+                    help="comma-separated workloads also timed (call, attention and combine launches) after "
+                         "the benchmark workload; empty skips them")
     ap.add_argument("--sweep", action="store_true",
                     help="instead of the benchmark: the dense-versus-dilated sweep over N = 8K..1M "
                          "(fixed tokens per batch), one JSON line per (N, variant)")
@@ -450,44 +454,11 @@ def main():
 
     flops = info["sparse_flops"]
     peak = PEAK_BF16_TFLOPS if wl.dtype == "bf16" else PEAK_F32_TFLOPS
-    fused = bool(info["combine_fused"])
-    ms, ms_first, ms_second = timed(args.steps)
+    ms, ms_attn, ms_comb = timed(args.steps)
     prof = profiled_counters(wl.name)
-
-    fused_path = None
-    if not fused and os.environ.get("DILATED_ATTN_FUSE_COMBINE") is None:
-        # The opt-in path with the combine in the r = 1 pattern's attention launch.
-        os.environ["DILATED_ATTN_FUSE_COMBINE"] = "1"
-        try:
-            if plan(wl.B, wl.N, wl.H, wl.D, pats, wl.causal, wl.torch_dtype)["combine_fused"]:
-                f_ms, f_first, f_second = timed(args.steps)
-                f_tf = flops / ((f_first + f_second) * 1e-3) / 1e12
-                fused_path = {
-                    "ms_per_step": round(f_ms, 5), "tflops": round(flops / (f_ms * 1e-3) / 1e12, 3),
-                    "launch_other_patterns_ms": round(f_first, 5),
-                    "launch_fused_pattern_with_combine_ms": round(f_second, 5),
-                    "attention_with_combine_tflops": round(f_tf, 3),
-                    "attention_with_combine_frac_of_mfma_peak": round(f_tf / peak, 4),
-                    "traffic": prof.get("fused_attention_bytes_per_call"),
-                    "mfma_busy_pct_profiled": prof.get("fused_attention_mfma_busy_pct")}
-        finally:
-            del os.environ["DILATED_ATTN_FUSE_COMBINE"]
-
     tflops = flops / (ms * 1e-3) / 1e12
-    if fused:
-        # Both launches run the attention kernel; the second also mixes the patterns.
-        ms_attn = ms_first + ms_second
-        traffic = prof.get("fused_attention_bytes_per_call")
-        busy = prof.get("fused_attention_mfma_busy_pct")
-        stages = {"launch_other_patterns_ms": round(ms_first, 5),
-                  "launch_fused_pattern_with_combine_ms": round(ms_second, 5)}
-    else:
-        ms_attn = ms_first
-        traffic = prof.get("attention_bytes_per_launch")
-        busy = prof.get("attention_mfma_busy_pct")
-        stages = {"attention_ms": round(ms_first, 5), "combine_ms": round(ms_second, 5)}
     attn_tflops = flops / (ms_attn * 1e-3) / 1e12
-    comb_gbs = info["bytes_combine"] / (ms_second * 1e-3) / 1e9
+    comb_gbs = info["bytes_combine"] / (ms_comb * 1e-3) / 1e9
     res = {
         "metric": METRIC,
         "value": round(tflops, 3),
@@ -504,18 +475,19 @@ def main():
         "config": wl.describe(),
         "tokens_per_s": round(wl.B * wl.N / (ms * 1e-3), 1),
         "sparse_flops": flops,
-        "combine_fused": fused,
-        "launches": stages,
+        "launches": {"attention_ms": round(ms_attn, 5), "combine_ms": round(ms_comb, 5)},
         "attention_stage": {"ms": round(ms_attn, 5), "tflops": round(attn_tflops, 3),
                             "frac_of_mfma_peak": round(attn_tflops / peak, 4),
-                            "mfma_busy_pct_profiled": busy},
-        "combine_stage": ({"fused_into_attention": True} if fused else
-                          {"ms": round(ms_second, 5), "algorithmic_bytes": info["bytes_combine"],
-                           "gbps": round(comb_gbs, 1), "frac_of_hbm_peak": round(comb_gbs / PEAK_HBM_GBS, 4),
-                           "traffic": prof.get("combine_bytes_per_launch")}),
-        "fused_combine_path": fused_path,
+                            "algorithmic_bytes": info["bytes_attn"],
+                            "mfma_busy_pct_profiled": prof.get("attention_mfma_busy_pct")},
+        "combine_stage": {"ms": round(ms_comb, 5), "algorithmic_bytes": info["bytes_combine"],
+                          "gbps": round(comb_gbs, 1), "frac_of_hbm_peak": round(comb_gbs / PEAK_HBM_GBS, 4),
+                          "traffic": prof.get("combine_bytes_per_launch"),
+                          "note": "workspace of this size can be held in the 256 MB Infinity Cache; "
+                                  "see large_workloads for the combine's HBM rate"},
         "roofline": {"bound": "mfma", "achieved": round(attn_tflops, 3), "peak": peak,
-                     "unit": "TFLOP/s", "frac": round(attn_tflops / peak, 4), "traffic": traffic},
+                     "unit": "TFLOP/s", "frac": round(attn_tflops / peak, 4),
+                     "traffic": prof.get("attention_bytes_per_launch")},
         "cpu_baseline": None,
     }
     if args.dist_steps > 0:
@@ -526,7 +498,67 @@ def main():
         }
     if args.cpu_seconds > 0:
         res["cpu_baseline"] = cpu_baseline(wl, q, k, v, args.cpu_seconds)
+    names = [n for n in args.large.split(",") if n and n != wl.name]
+    if names:
+        del q, k, v, out, lse, ws
+        torch.cuda.empty_cache()
+        res["large_workloads"] = [large_workload(workloads.BY_NAME[n], args) for n in names]
     print(json.dumps(res), flush=True)
+
+
+def large_workload(wl, args):
+    """One more workload: mean ms per call over back-to-back calls after the
+    warm-up, then the mean of each launch over as many calls (events recorded
+    by the library around its two launches), the attention launch against
+    the MFMA peak and the combine launch's algorithmic bytes against the HBM
+    peak.  Its workspace is far larger than the Infinity Cache."""
+    import torch
+
+    import workloads
+    from paper_2307_02486_amd import StageTimer, dilated_attn, plan, workspace_for
+    dev = torch.device("cuda:0")
+    stream = torch.cuda.current_stream(dev)
+    q, k, v = workloads.make_qkv(wl, device=dev)
+    pats = list(wl.patterns)
+    info = plan(wl.B, wl.N, wl.H, wl.D, pats, wl.causal, wl.torch_dtype)
+    out = torch.empty_like(q)
+    lse = torch.empty((wl.B, wl.H, wl.N), dtype=torch.float32, device=dev)
+    ws = workspace_for(q, pats, wl.causal)
+
+    def step():
+        dilated_attn(q, k, v, pats, wl.causal, out=out, lse=lse, workspace=ws, stream=stream)
+
+    t0, n = time.perf_counter(), 0
+    while n < 3 or time.perf_counter() - t0 < args.warmup_seconds:
+        step()
+        n += 1
+        torch.cuda.synchronize()
+    calls = max(3, min(args.steps, int(2000.0 / max(1.0, 1e3 * (time.perf_counter() - t0) / n))))
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    e0.record(stream)
+    for _ in range(calls):
+        step()
+    e1.record(stream)
+    torch.cuda.synchronize()
+    ms = e0.elapsed_time(e1) / calls
+    with StageTimer(capacity=calls) as st:
+        for _ in range(calls):
+            step()
+        torch.cuda.synchronize()
+    ms_attn, ms_comb = st.ms_attention / st.calls, st.ms_combine / st.calls
+    flops = info["sparse_flops"]
+    attn_tflops = flops / (ms_attn * 1e-3) / 1e12
+    comb_gbs = info["bytes_combine"] / (ms_comb * 1e-3) / 1e9
+    rec = {"config": wl.describe(), "calls": calls, "ms_per_call": round(ms, 4),
+           "tflops": round(flops / (ms * 1e-3) / 1e12, 3), "tokens_per_s": round(wl.B * wl.N / (ms * 1e-3), 1),
+           "sparse_flops": flops, "workspace_bytes": info["workspace_bytes"],
+           "attention_stage": {"ms": round(ms_attn, 4), "tflops": round(attn_tflops, 3),
+                               "frac_of_mfma_peak": round(attn_tflops / PEAK_BF16_TFLOPS, 4)},
+           "combine_stage": {"ms": round(ms_comb, 4), "algorithmic_bytes": info["bytes_combine"],
+                             "gbps": round(comb_gbs, 1), "frac_of_hbm_peak": round(comb_gbs / PEAK_HBM_GBS, 4)}}
+    del q, k, v, out, lse, ws
+    torch.cuda.empty_cache()
+    return rec
 
 
 if __name__ == "__main__":

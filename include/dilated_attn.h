@@ -72,17 +72,10 @@ typedef struct {
                                Sec. 2.4 counted exactly                       */
   double bytes_attn;        /* algorithmic HBM bytes of the attention stage:
                                kept q/k/v rows read once, per-pattern output
-                               and lse written once                          */
+                               rows and their 8-byte records written once    */
   double bytes_combine;     /* algorithmic HBM bytes of the combine stage:
-                               per-pattern output and lse read once, out and
-                               lse written once                               */
-  int64_t combine_fused;    /* 1: fwd runs the combine inside the attention
-                               kernel of the first pattern with r = 1, as a
-                               second attention launch after the other
-                               patterns'; opt-in, with the environment
-                               variable DILATED_ATTN_FUSE_COMBINE = "1", for
-                               bf16 inputs and D <= 64.  0: a separate
-                               combine kernel (the default)                  */
+                               per-pattern output rows and records read once,
+                               out and lse written once                       */
 } da_plan_info_t;
 
 /*
@@ -115,6 +108,14 @@ int dilated_attn_plan(int64_t B, int64_t N, int64_t H, int64_t D,
  * All device pointers must be 16-byte aligned and out must not overlap q, k
  * or v.  Returns DA_OK or a negative error code; before any launch, every
  * argument is checked and an error leaves all buffers untouched.
+ *
+ * Arithmetic for DA_BF16: scores q.k as exact bf16 products summed in
+ * float32, times softmax_scale*log2(e) in float32; probabilities rounded to
+ * bf16 for the product with v (float32 sums); each pattern's normalised rows
+ * kept in the workspace as fp16 divided by a power of two per row, within
+ * 2^-11 of the row's largest magnitude; the mixture in float32; out rounded
+ * once to bf16.  Results are finite whenever every scaled score is finite in
+ * float32 and max|v| < 2^95.  DA_F32 computes in float32 throughout.
  */
 int dilated_attn_fwd(const void* q, const void* k, const void* v, void* out,
                      float* lse, int64_t B, int64_t N, int64_t H, int64_t D,
@@ -318,10 +319,8 @@ const char* dilated_attn_strerror(int code);
  * current device; each of the next `capacity` dilated_attn_fwd calls records
  * one event before its first launch, one between its two launches and one
  * after the second, on the call's stream (calls beyond capacity are not
- * timed).  The two launches are the attention stage and the combine stage,
- * or, with the combine fused (da_plan_info_t.combine_fused), the attention
- * launch of every pattern but the fused one and the attention launch of the
- * fused pattern with the combine.  dilated_attn_profile_end waits for the recorded events, writes the
+ * timed).  The two launches are the attention stage and the combine stage.
+ * dilated_attn_profile_end waits for the recorded events, writes the
  * summed durations of the two stages in milliseconds and the number of timed
  * calls, and destroys the events.  capacity must be in [1, 1<<20]; any
  * pointer argument of profile_end may be NULL.  Not thread safe: one profiling

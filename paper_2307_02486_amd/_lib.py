@@ -31,8 +31,7 @@ class PlanInfo(ctypes.Structure):
                 ("covered_rows", ctypes.c_int64),
                 ("sparse_flops", ctypes.c_double),
                 ("bytes_attn", ctypes.c_double),
-                ("bytes_combine", ctypes.c_double),
-                ("combine_fused", ctypes.c_int64)]
+                ("bytes_combine", ctypes.c_double)]
 
 
 class DilatedAttnError(RuntimeError):

@@ -53,7 +53,6 @@ int dilated_attn_plan(int64_t B, int64_t N, int64_t H, int64_t D, const da_patte
   info->sparse_flops = p.sparse_flops;
   info->bytes_attn = p.bytes_attn;
   info->bytes_combine = p.bytes_combine;
-  info->combine_fused = p.fuse >= 0 ? 1 : 0;
   return DA_OK;
 }
 
@@ -86,19 +85,9 @@ int dilated_attn_fwd(const void* q, const void* k, const void* v, void* out, flo
   hipEvent_t* ev = nullptr;
   if (g_prof.active && g_prof.used < g_prof.capacity) ev = &g_prof.ev[3 * g_prof.used++];
   if (ev && hipEventRecord(ev[0], s) != hipSuccess) return DA_EHIP;
-  if (p.fuse >= 0) {
-    // every pattern but the fused one, then the fused one with the combine
-    if (da::launch_attention(p, da::kOtherPatterns, q, k, v, workspace, out, lse, s) != hipSuccess)
-      return DA_EHIP;
-    if (ev && hipEventRecord(ev[1], s) != hipSuccess) return DA_EHIP;
-    if (da::launch_attention(p, da::kFusedPattern, q, k, v, workspace, out, lse, s) != hipSuccess)
-      return DA_EHIP;
-  } else {
-    if (da::launch_attention(p, da::kAllPatterns, q, k, v, workspace, out, lse, s) != hipSuccess)
-      return DA_EHIP;
-    if (ev && hipEventRecord(ev[1], s) != hipSuccess) return DA_EHIP;
-    if (da::launch_combine(p, workspace, out, lse, s) != hipSuccess) return DA_EHIP;
-  }
+  if (da::launch_attention(p, q, k, v, workspace, s) != hipSuccess) return DA_EHIP;
+  if (ev && hipEventRecord(ev[1], s) != hipSuccess) return DA_EHIP;
+  if (da::launch_combine(p, workspace, out, lse, s) != hipSuccess) return DA_EHIP;
   if (ev && hipEventRecord(ev[2], s) != hipSuccess) return DA_EHIP;
   return DA_OK;
 }
@@ -119,7 +108,6 @@ int dilated_attn_bwd_plan(int64_t B, int64_t N, int64_t H, int64_t D, const da_p
   info->sparse_flops = l.flops;
   info->bytes_attn = l.bytes_grad;
   info->bytes_combine = l.bytes_combine;
-  info->combine_fused = 0;
   return DA_OK;
 }
 

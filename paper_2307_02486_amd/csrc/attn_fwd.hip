@@ -2,8 +2,8 @@
 // (batch, head, segment), gather the kept rows (every r-th row from the head's
 // offset, Sec. 2.2 Eqs. 3-5 and Sec. 2.3) straight from HBM into LDS, and run
 // softmax attention on them (Sec. 2.2 Eq. 6) with an online softmax.  The
-// normalised output rows and their log-sum-exp go to the workspace in compact
-// per-pattern order [b][h][segment][t][D].
+// normalised output rows go to the workspace in compact per-pattern order
+// [b][h][segment][t][D], with one (lse, scale) record per row.
 //
 // bf16 path: one work item = 128 query rows of one sparsified segment, four
 // waves of 32 rows.  Scores are computed transposed, S^T = K Q^T, with
@@ -32,16 +32,10 @@ struct AttnArgs {
   const void* v;
   char* ws;
   int32_t B, N, H, npat, causal, total_items;
-  float scale_log2;  // softmax scale times log2(e): scores go to exp2 directly
+  float scale_log2;  // softmax scale times log2(e), applied to the fp32 scores
   // The patterns of this launch, ordered by query tiles per unit, most first
   // (the kernels only use a pattern's index to find its record here).
   PatArgs pat[DA_MAX_PATTERNS];
-  // Fused combine only: out, lse and every pattern of the call in the call's
-  // order; mix[fuse] is the pattern this launch computes.
-  void* out;
-  float* lse;
-  int32_t mix_npat, fuse;
-  MixPat mix[DA_MAX_PATTERNS];
 };
 
 // ---------------------------------------------------------------------------
@@ -75,11 +69,23 @@ struct SmemBf16 {
   int redo;  // set by a wave whose tile sums left the fast path's range
 };
 
-// kMixNP = 0: the per-pattern rows go to the workspace.  kMixNP > 0: this
-// launch computes a pattern with r = 1 after every other pattern's rows are
-// in the workspace, and its epilogue mixes them (kMixNP >= the call's pattern
-// count bounds the mixing loops at compile time: 4, 5, 8 or 16).
-template <int D, bool kBufferLoads, int kMixNP>
+// The per-pattern output rows are stored as fp16 scaled by a power of two
+// per row: row t of a work item holds O_t * 2^-e_t with e_t chosen so that
+// the row's largest magnitude lands in [2^14, 2^15), and its record holds
+// (lse_t, 2^e_t).  The rows keep fp16's eleven significant bits relative to
+// the row's largest element and bf16's exponent range (Eq. 6 puts no bound
+// on the magnitude of a row).
+__device__ inline void row_scale(float amax_times_inv, float inv, float& mul, float& stored) {
+  // biased exponent E of the normalised row max a: a in [2^(E-127), 2^(E-126));
+  // a * 2^(141-E) is in [2^14, 2^15).  E is clamped to [15, 254] so that both
+  // powers of two are normal floats (rows below 2^-111 keep fewer bits).
+  int E = static_cast<int>((__builtin_bit_cast(unsigned, amax_times_inv) >> 23) & 0xff);
+  E = min(max(E, 15), 254);
+  mul = inv * __builtin_bit_cast(float, static_cast<unsigned>(268 - E) << 23);     // inv * 2^(141-E)
+  stored = __builtin_bit_cast(float, static_cast<unsigned>(E - 14) << 23);         // 2^(E-141)
+}
+
+template <int D, bool kBufferLoads>
 __global__ __launch_bounds__(kThreads) void attn_fwd_bf16(AttnArgs a) {
   static_assert(D % 32 == 0, "head dim must be a multiple of 32");
   constexpr int BN = kBN;
@@ -108,12 +114,13 @@ __global__ __launch_bounds__(kThreads) void attn_fwd_bf16(AttnArgs a) {
   const int tq_row = q0 + wv * 32 + qr;  // this lane's query (kept-row index)
   const bool q_valid = tq_row < L;
   const int64_t row_step = it.rstride * D;  // elements between consecutive kept rows
+  const float c = a.scale_log2;             // > 0
 
   // Q^T operand: lane holds query tq_row, head-dim slice [16c + 8hi, +8).  The
   // loads are issued here and consumed after the first K/V tile's loads have
   // been issued, so the two latencies overlap.
   // Rows past the segment's end load its last row (unconditional loads, no
-  // branches) and are zeroed at the conversion.
+  // branches) and are zeroed before use.
   u32x4 qraw[KC];
   {
     const int qrow = min(tq_row, L - 1);
@@ -190,28 +197,24 @@ __global__ __launch_bounds__(kThreads) void attn_fwd_bf16(AttnArgs a) {
     }
 
   load_tile(0, 0);
-  // Q multiplied by scale * log2(e) and rounded to bf16: the MFMA then yields
-  // scores in log2 units and the exponent needs no per-score multiply.
+  // Q enters the MFMA exactly as given (bf16): the softmax scale is applied to
+  // the fp32 scores, so no second rounding of q enters them.
   bf16x8 qreg[KC];
 #pragma unroll
-  for (int c = 0; c < KC; ++c)
-#pragma unroll
-    for (int e = 0; e < 8; ++e) {
-      const unsigned bits = q_valid ? (qraw[c][e >> 1] >> (16 * (e & 1))) << 16 : 0u;
-      qreg[c][e] = (__bf16)(__builtin_bit_cast(float, bits) * a.scale_log2);
-    }
+  for (int c = 0; c < KC; ++c) {
+    const u32x4 x = q_valid ? qraw[c] : u32x4{0u, 0u, 0u, 0u};
+    qreg[c] = __builtin_bit_cast(bf16x8, x);
+  }
   if (tid == 0) sm.redo = 0;
 
   f32x16 acc_o[DB];
-  float m_run, l_run;  // reference max (log2 domain) and this half-wave's share of the denominator
-  f32x16 negm;         // -m_run in every slot: the initial value of each S' block
+  float m_run, l_run;  // reference max (log2 units) and this half-wave's share of the denominator
   bool safe = false;   // safe mode: a row max for every tile
   for (;;) {
 #pragma unroll
   for (int db = 0; db < DB; ++db) acc_o[db] = f32x16{};
   m_run = 0.0f;
   l_run = 0.0f;
-  negm = f32x16{};
   __builtin_amdgcn_s_waitcnt(kWaitVmcnt0);
   __syncthreads();
   for (int jt = 0; jt < ntile; ++jt) {
@@ -224,8 +227,9 @@ __global__ __launch_bounds__(kThreads) void attn_fwd_bf16(AttnArgs a) {
 
     // Tiles entirely after this wave's queries are skipped (causal).
     if (!(a.causal && k0 > wq_lo + 31)) {
-      // S^T = K Q^T, one 32x32 block per 32 keys; the K fragments of a group
-      // of QG blocks are requested from LDS before the group's MFMAs.
+      // S^T = K Q^T (unscaled fp32 scores), one 32x32 block per 32 keys; the
+      // K fragments of a group of QG blocks are requested from LDS before the
+      // group's MFMAs.
       constexpr int QG = (D <= 64 ? SB : 1);
       f32x16 acc_s[SB];
 #pragma unroll
@@ -239,7 +243,7 @@ __global__ __launch_bounds__(kThreads) void attn_fwd_bf16(AttnArgs a) {
         __builtin_amdgcn_sched_barrier(0);  // keep the reads ahead of the MFMAs
 #pragma unroll
         for (int g = 0; g < QG; ++g) {
-          acc_s[kb0 + g] = negm;  // scores start at -m: S' = q'k - m
+          acc_s[kb0 + g] = f32x16{};
 #pragma unroll
           for (int c = 0; c < KC; ++c)
             acc_s[kb0 + g] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(__builtin_bit_cast(bf16x8, kf[g][c]),
@@ -263,7 +267,7 @@ __global__ __launch_bounds__(kThreads) void attn_fwd_bf16(AttnArgs a) {
         for (int kb = 0; kb < SB; ++kb)
 #pragma unroll
           for (int j = 0; j < 16; j += 2) mx = fmaxf(mx, fmaxf(acc_s[kb][j], acc_s[kb][j + 1]));
-        mx = fmaxf(mx, other_half(mx));  // already relative to m_run, log2 units
+        mx = fmaxf(mx, other_half(mx)) * c - m_run;  // log2 units, relative to m_run
         // The first tile fixes the reference max; in the safe mode later tiles
         // move it only when some row of the wave would see probabilities above
         // 2^kRescaleSlack.
@@ -276,21 +280,16 @@ __global__ __launch_bounds__(kThreads) void attn_fwd_bf16(AttnArgs a) {
           for (int db = 0; db < DB; ++db)
 #pragma unroll
             for (int j = 0; j < 16; ++j) acc_o[db][j] *= alpha;
-#pragma unroll
-          for (int kb = 0; kb < SB; ++kb)
-#pragma unroll
-            for (int j = 0; j < 16; ++j) acc_s[kb][j] -= delta;
-#pragma unroll
-          for (int j = 0; j < 16; ++j) negm[j] = -m_run;
         }
       }
-      // P = exp2(S'); bf16 P feeds the PV MFMA.  Row sums are taken in fp32
-      // with plain adds (dot-product instructions would not issue while other
-      // waves' MFMAs run).  The A operand V^T comes from the row-major V tile
-      // through transposed LDS reads: for MFMA step (kb, kk) the lane's eight
-      // keys are kb*32 + 16kk + 4hi + {0..3} and the same + 8, matching the
-      // keys its half-wave holds in S^T.
-      float lp[4] = {0.0f, 0.0f, 0.0f, 0.0f};
+      // P = exp2(c S - m); bf16 P feeds the PV MFMA.  Row sums are taken in
+      // fp32 with plain adds (dot-product instructions would not issue while
+      // other waves' MFMAs run).  The A operand V^T comes from the row-major V
+      // tile through transposed LDS reads: for MFMA step (kb, kk) the lane's
+      // eight keys are kb*32 + 16kk + 4hi + {0..3} and the same + 8, matching
+      // the keys its half-wave holds in S^T.
+      const float negm = -m_run;
+      float lp[4];
       const uint32_t vaddr = lds_addr(vl);
       static_for<0, SB>([&](auto KB) {
         constexpr int kb = decltype(KB)::value;
@@ -311,8 +310,9 @@ __global__ __launch_bounds__(kThreads) void attn_fwd_bf16(AttnArgs a) {
           bf16x8 pb;
 #pragma unroll
           for (int e = 0; e < 8; ++e) {
-            const float pe = __builtin_amdgcn_exp2f(acc_s[kb][8 * kk + e]);
-            lp[e & 3] += pe;
+            const float pe = __builtin_amdgcn_exp2f(__builtin_fmaf(acc_s[kb][8 * kk + e], c, negm));
+            if (kb == 0 && kk == 0 && e < 4) lp[e] = pe;
+            else lp[e & 3] += pe;
             pb[e] = (__bf16)pe;
           }
           lds_wait<(1 - kk) * 2 * DB>();  // step kk's reads done, the later step's may be pending
@@ -344,8 +344,6 @@ __global__ __launch_bounds__(kThreads) void attn_fwd_bf16(AttnArgs a) {
           for (int db = 0; db < DB; ++db)
 #pragma unroll
             for (int j = 0; j < 16; ++j) acc_o[db][j] *= alpha;
-#pragma unroll
-          for (int j = 0; j < 16; ++j) negm[j] = -m_run;
         }
       }
     }
@@ -362,14 +360,23 @@ __global__ __launch_bounds__(kThreads) void attn_fwd_bf16(AttnArgs a) {
   load_tile(0, 0);
   }
 
-  // Epilogue: normalise this wave's 32 rows of the per-pattern output and
-  // stage them in a private LDS region (the tiles are no longer read: the
-  // loop ended with a barrier), so that the stores write whole rows, 16
-  // bytes per lane.  Staged 16-byte chunk x of row k sits at chunk
-  // x ^ ((k >> 1) mod D/8): the 8-byte writes (one row per lane) then hit at
-  // most two lanes per bank pair and the 16-byte reads none.
+  // Epilogue: normalise this wave's 32 rows of the per-pattern output, scale
+  // each row by its power of two and stage the fp16 rows in a private LDS
+  // region (the tiles are no longer read: the loop ended with a barrier), so
+  // that the stores write whole rows, 16 bytes per lane.  Staged 16-byte
+  // chunk x of row k sits at chunk x ^ ((k >> 1) mod D/8): the 8-byte writes
+  // (one row per lane) then hit at most two lanes per bank pair and the
+  // 16-byte reads none.
   const float l_tot = l_run + other_half(l_run);
   const float inv = 1.0f / l_tot;
+  float amax = 0.0f;
+#pragma unroll
+  for (int db = 0; db < DB; ++db)
+#pragma unroll
+    for (int j = 0; j < 16; ++j) amax = fmaxf(amax, fabsf(acc_o[db][j]));
+  amax = fmaxf(amax, other_half(amax));
+  float mul, rscale;
+  row_scale(amax * inv, inv, mul, rscale);
   char* stg = reinterpret_cast<char*>(&sm.k[0][0]) + wv * 32 * TL::kRowBytes;
   auto stg_off = [&](int row, int chunk) {
     return row * TL::kRowBytes + ((chunk ^ ((row >> 1) & (TL::kSlots - 1))) << 4);
@@ -380,104 +387,21 @@ __global__ __launch_bounds__(kThreads) void attn_fwd_bf16(AttnArgs a) {
     for (int jj = 0; jj < 4; ++jj) {
       f16x4 o;
 #pragma unroll
-      for (int e = 0; e < 4; ++e) o[e] = (_Float16)(acc_o[db][4 * jj + e] * inv);
+      for (int e = 0; e < 4; ++e) o[e] = (_Float16)(acc_o[db][4 * jj + e] * mul);
       *reinterpret_cast<f16x4*>(stg + stg_off(qr, db * 4 + jj) + 8 * hi) = o;
     }
   const float lse_own = (m_run + __builtin_amdgcn_logf(l_tot)) * kLn2;
   // Each pass covers 64 consecutive 16-byte chunks: 1024 / (2 D) rows.
   constexpr int kPasses = 32 * TL::kRowBytes / 1024;
-  if constexpr (kMixNP == 0) {
-    if (hi == 0 && q_valid)
-      reinterpret_cast<float*>(a.ws + P.lse_off)[(int64_t)it.unit * P.lmax + tq_row] = lse_own;
-    _Float16* obase = reinterpret_cast<_Float16*>(a.ws + P.o_off) + ((int64_t)it.unit * P.lmax + wq_lo) * D;
+  if (hi == 0 && q_valid)
+    reinterpret_cast<f32x2*>(a.ws + P.lse_off)[(int64_t)it.unit * P.lmax + tq_row] = f32x2{lse_own, rscale};
+  _Float16* obase = reinterpret_cast<_Float16*>(a.ws + P.o_off) + ((int64_t)it.unit * P.lmax + wq_lo) * D;
 #pragma unroll
-    for (int i = 0; i < kPasses; ++i) {
-      const int row = (i * 64 + lane) / TL::kSlots;
-      const int chunk = (i * 64 + lane) % TL::kSlots;
-      const u32x4 x = *reinterpret_cast<const u32x4*>(stg + stg_off(row, chunk));
-      if (wq_lo + row < L) *reinterpret_cast<u32x4*>(obase + row * D + chunk * 8) = x;
-    }
-  } else {
-    // Fused combine (Sec. 2.2, Eqs. 7-10).  This pattern has r = 1, so kept
-    // row t of the segment is position p0 + t and every position of the
-    // sequence is some item's row.  Each lane takes 16-byte chunks of the
-    // wave's staged rows, loads the same chunk of every other pattern that
-    // keeps the position (with its lse) from the workspace, and mixes them
-    // exactly as the separate combine kernel does, in the call's pattern
-    // order: the two paths give identical results.
-    float* lse_stg = reinterpret_cast<float*>(&sm.v[0][0]) + wv * 32;
-    if (hi == 0) lse_stg[qr] = lse_own;
-    constexpr int NP = kMixNP;
-    // Passes whose loads are in flight together: all of them for up to 5
-    // patterns (one round of memory latency), else as many as 16 pattern
-    // slots allow (more would cost occupancy).
-    constexpr int PG = NP >= 16 ? 1 : (NP <= 5 ? kPasses : 16 / NP);
-    const int64_t bh = (int64_t)it.b * a.H + it.h;
-#pragma unroll
-    for (int i0 = 0; i0 < kPasses; i0 += PG) {
-      f16x8 ow[PG][NP];
-      float lw[PG][NP];
-#pragma unroll
-      for (int ip = 0; ip < PG; ++ip) {
-        const int i = i0 + ip;
-        const int row = (i * 64 + lane) / TL::kSlots;
-        const int chunk = (i * 64 + lane) % TL::kSlots;
-        const uint32_t p = static_cast<uint32_t>(it.p0 + wq_lo + row);
-        const bool valid = i < kPasses && wq_lo + row < L;
-#pragma unroll
-        for (int j = 0; j < NP; ++j) {
-          lw[ip][j] = -INFINITY;
-          if (j >= a.mix_npat || j == a.fuse || !valid) continue;
-          const MixPat& M = a.mix[j];
-          const uint32_t g = M.fw.div(p);
-          const uint32_t pos = p - g * M.fw.d;
-          const uint32_t t = M.fr.div(pos);
-          const uint32_t sj = static_cast<uint32_t>(it.h) - M.fr.div(static_cast<uint32_t>(it.h)) * M.fr.d;
-          if (pos - t * M.fr.d != sj) continue;
-          const int64_t wrow = (bh * M.nseg + g) * M.lmax + t;
-          // plain loads: the previous launch just wrote these rows, and part
-          // of them is still held in the L2 and the Infinity Cache
-          lw[ip][j] = reinterpret_cast<const float*>(a.ws + M.lse_off)[wrow];
-          ow[ip][j] = *reinterpret_cast<const f16x8*>(reinterpret_cast<const _Float16*>(a.ws + M.o_off) + wrow * D + chunk * 8);
-        }
-      }
-#pragma unroll
-      for (int ip = 0; ip < PG; ++ip) {
-        const int i = i0 + ip;
-        const int row = (i * 64 + lane) / TL::kSlots;
-        const int chunk = (i * 64 + lane) % TL::kSlots;
-        if (!(i < kPasses && wq_lo + row < L)) continue;
-        const int p = it.p0 + wq_lo + row;
-        const f16x8 own = *reinterpret_cast<const f16x8*>(stg + stg_off(row, chunk));
-        const float l0 = lse_stg[row];
-        float m = -INFINITY;
-#pragma unroll
-        for (int j = 0; j < NP; ++j) m = fmaxf(m, j == a.fuse ? l0 : lw[ip][j]);
-        float den = 0.0f;
-        f32x8 acc = f32x8{0, 0, 0, 0, 0, 0, 0, 0};
-#pragma unroll
-        for (int j = 0; j < NP; ++j) {
-          const bool mine = j == a.fuse;
-          const float lj = mine ? l0 : lw[ip][j];
-          if (lj == -INFINITY) continue;
-          const float e = __builtin_amdgcn_exp2f((lj - m) * kLog2e);
-          den += e;
-          const f16x8 oj = mine ? own : ow[ip][j];
-          f32x8 of;
-#pragma unroll
-          for (int x = 0; x < 8; ++x) of[x] = static_cast<float>(oj[x]);
-          acc += e * of;
-        }
-        acc *= 1.0f / den;
-        bf16x8 ob;
-#pragma unroll
-        for (int x = 0; x < 8; ++x) ob[x] = (__bf16)acc[x];
-        u16* orow = static_cast<u16*>(a.out) + (((int64_t)it.b * a.N + p) * a.H + it.h) * D + chunk * 8;
-        __builtin_nontemporal_store(ob, reinterpret_cast<bf16x8*>(orow));
-        if (chunk == 0)
-          __builtin_nontemporal_store(m + __builtin_amdgcn_logf(den) * kLn2, a.lse + bh * a.N + p);
-      }
-    }
+  for (int i = 0; i < kPasses; ++i) {
+    const int row = (i * 64 + lane) / TL::kSlots;
+    const int chunk = (i * 64 + lane) % TL::kSlots;
+    const u32x4 x = *reinterpret_cast<const u32x4*>(stg + stg_off(row, chunk));
+    if (wq_lo + row < L) *reinterpret_cast<u32x4*>(obase + row * D + chunk * 8) = x;
   }
 }
 
@@ -568,40 +492,14 @@ __global__ __launch_bounds__(kBM32) void attn_fwd_f32(AttnArgs a) {
 #pragma unroll
   for (int d = 0; d < D; d += 4)
     *reinterpret_cast<f32x4*>(orow + d) = f32x4{o[d] * inv, o[d + 1] * inv, o[d + 2] * inv, o[d + 3] * inv};
-  reinterpret_cast<float*>(a.ws + P.lse_off)[wrow] = (m_run + __builtin_amdgcn_logf(l_run)) * kLn2;
+  // float32 rows need no scale: the record's scale is 1
+  reinterpret_cast<f32x2*>(a.ws + P.lse_off)[wrow] = f32x2{(m_run + __builtin_amdgcn_logf(l_run)) * kLn2, 1.0f};
 }
 
 }  // namespace
 
-namespace {
-
-// The plan fuses the combine only for D <= 64.
-template <int D, bool kBuf>
-hipError_t launch_bf16(const dim3& grid, hipStream_t stream, const AttnArgs& a, bool fused) {
-  if (!fused) {
-    hipLaunchKernelGGL((attn_fwd_bf16<D, kBuf, 0>), grid, dim3(kThreads), 0, stream, a);
-  } else if constexpr (D <= 64) {
-    if (a.mix_npat <= 4)
-      hipLaunchKernelGGL((attn_fwd_bf16<D, kBuf, 4>), grid, dim3(kThreads), 0, stream, a);
-    else if (a.mix_npat <= 5)
-      hipLaunchKernelGGL((attn_fwd_bf16<D, kBuf, 5>), grid, dim3(kThreads), 0, stream, a);
-    else if (a.mix_npat <= 8)
-      hipLaunchKernelGGL((attn_fwd_bf16<D, kBuf, 8>), grid, dim3(kThreads), 0, stream, a);
-    else
-      hipLaunchKernelGGL((attn_fwd_bf16<D, kBuf, DA_MAX_PATTERNS>), grid, dim3(kThreads), 0, stream, a);
-  } else {
-    return hipErrorInvalidValue;
-  }
-  return hipSuccess;
-}
-
-}  // namespace
-
-hipError_t launch_attention(const Plan& plan, AttnPart part, const void* q, const void* k,
-                            const void* v, void* workspace, void* out, float* lse,
-                            hipStream_t stream) {
-  const bool fused = part == kFusedPattern;
-  if (part != kAllPatterns && (plan.fuse < 0 || plan.dtype != DA_BF16)) return hipErrorInvalidValue;
+hipError_t launch_attention(const Plan& plan, const void* q, const void* k, const void* v,
+                            void* workspace, hipStream_t stream) {
   AttnArgs a;
   a.q = q;
   a.k = k;
@@ -612,19 +510,10 @@ hipError_t launch_attention(const Plan& plan, AttnPart part, const void* q, cons
   a.H = static_cast<int32_t>(plan.H);
   a.causal = plan.causal;
   a.scale_log2 = plan.scale * kLog2e;
-  a.out = out;
-  a.lse = lse;
-  a.mix_npat = plan.npat;
-  a.fuse = plan.fuse;
-  for (int i = 0; i < DA_MAX_PATTERNS; ++i)
-    a.mix[i] = i < plan.npat ? make_mixpat(plan.pat[i]) : MixPat{make_fastdiv(1), make_fastdiv(1), 1, 1, 0, 0};
-  // The patterns of this launch, most query tiles per unit first.
+  // The patterns of the launch, most query tiles per unit first.
   int order[DA_MAX_PATTERNS];
-  int n = 0;
-  for (int i = 0; i < plan.npat; ++i) {
-    const bool mine = part == kAllPatterns || (part == kFusedPattern) == (i == plan.fuse);
-    if (mine) order[n++] = i;
-  }
+  const int n = plan.npat;
+  for (int i = 0; i < n; ++i) order[i] = i;
   std::stable_sort(order, order + n, [&](int x, int y) { return plan.pat[x].ntiles > plan.pat[y].ntiles; });
   a.npat = n;
   int64_t items = 0, launch = 0;
@@ -651,23 +540,21 @@ hipError_t launch_attention(const Plan& plan, AttnPart part, const void* q, cons
   if (items == 0) return hipSuccess;
   const dim3 grid(static_cast<unsigned>(launch));
   if (plan.dtype == DA_BF16) {
-    hipError_t e;
     switch (plan.D) {
       case 32:
-        e = plan.offsets32 ? launch_bf16<32, true>(grid, stream, a, fused)
-                           : launch_bf16<32, false>(grid, stream, a, fused);
+        if (plan.offsets32) hipLaunchKernelGGL((attn_fwd_bf16<32, true>), grid, dim3(kThreads), 0, stream, a);
+        else hipLaunchKernelGGL((attn_fwd_bf16<32, false>), grid, dim3(kThreads), 0, stream, a);
         break;
       case 64:
-        e = plan.offsets32 ? launch_bf16<64, true>(grid, stream, a, fused)
-                           : launch_bf16<64, false>(grid, stream, a, fused);
+        if (plan.offsets32) hipLaunchKernelGGL((attn_fwd_bf16<64, true>), grid, dim3(kThreads), 0, stream, a);
+        else hipLaunchKernelGGL((attn_fwd_bf16<64, false>), grid, dim3(kThreads), 0, stream, a);
         break;
       case 128:
-        e = plan.offsets32 ? launch_bf16<128, true>(grid, stream, a, fused)
-                           : launch_bf16<128, false>(grid, stream, a, fused);
+        if (plan.offsets32) hipLaunchKernelGGL((attn_fwd_bf16<128, true>), grid, dim3(kThreads), 0, stream, a);
+        else hipLaunchKernelGGL((attn_fwd_bf16<128, false>), grid, dim3(kThreads), 0, stream, a);
         break;
       default: return hipErrorInvalidValue;
     }
-    if (e != hipSuccess) return e;
   } else {
     switch (plan.D) {
       case 32: hipLaunchKernelGGL(attn_fwd_f32<32>, grid, dim3(kBM32), 0, stream, a); break;

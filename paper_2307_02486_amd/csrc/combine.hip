@@ -9,6 +9,8 @@
 // lane owns eight consecutive head-dim elements of one row, so a row of a
 // per-pattern output is read with D/8 16-byte (fp16) or 32-byte (fp32) loads
 // and consecutive positions of a dense pattern are consecutive in memory.
+// A per-pattern row is stored divided by a power of two (its record's
+// scale), which multiplies the row's weight.
 // Whether pattern i keeps row p for head h, and at which compact index t,
 // follows from g = p div w, t = (p - g w) div r and (p - g w) mod r ==
 // h mod r, with the divisions done by multiply-shift constants prepared on
@@ -21,6 +23,7 @@ namespace da {
 namespace {
 
 typedef float f32x4 __attribute__((ext_vector_type(4)));
+typedef float f32x2 __attribute__((ext_vector_type(2)));
 typedef float f32x8 __attribute__((ext_vector_type(8)));
 typedef _Float16 f16x8 __attribute__((ext_vector_type(8)));
 typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
@@ -43,7 +46,7 @@ template <typename WsT> struct Vec8;
 template <> struct Vec8<_Float16> { typedef f16x8 type; };
 template <> struct Vec8<float> { typedef f32x8 type; };
 
-// Workspace rows and lse values are read exactly once, but the attention
+// Workspace rows and records are read exactly once, but the attention
 // launch just wrote them and part of them is still held in the L2 and the
 // Infinity Cache: plain loads, which can hit there (nontemporal loads
 // measured 9 % slower on the 32K-token workload, equal at 256K).
@@ -94,7 +97,7 @@ __global__ __launch_bounds__(kThreads) void combine_fwd(CombArgs a) {
 
   // Issue the loads of every pattern that keeps each of this lane's rows.
   typename Vec8<WsT>::type o[kRows][NP];
-  float li[kRows][NP];
+  float li[kRows][NP], sc[kRows][NP];
 #pragma unroll
   for (int k = 0; k < kRows; ++k) {
     const int p = p0 + k * RPB;
@@ -109,7 +112,9 @@ __global__ __launch_bounds__(kThreads) void combine_fwd(CombArgs a) {
       const uint32_t s = static_cast<uint32_t>(h) - P.fr.div(static_cast<uint32_t>(h)) * P.fr.d;
       if (pos - t * P.fr.d != s) continue;
       const int64_t row = ((int64_t)bh * P.nseg + g) * P.lmax + t;
-      li[k][i] = reinterpret_cast<const float*>(a.ws + P.lse_off)[row];
+      const f32x2 rec = reinterpret_cast<const f32x2*>(a.ws + P.lse_off)[row];
+      li[k][i] = rec[0];
+      sc[k][i] = rec[1];
       o[k][i] = load8(reinterpret_cast<const WsT*>(a.ws + P.o_off) + row * D + d0);
     }
   }
@@ -131,7 +136,7 @@ __global__ __launch_bounds__(kThreads) void combine_fwd(CombArgs a) {
         if (li[k][i] == -INFINITY) continue;
         const float e = __builtin_amdgcn_exp2f((li[k][i] - m) * kLog2e);
         den += e;
-        acc += e * to_f32(o[k][i]);
+        acc += (e * sc[k][i]) * to_f32(o[k][i]);
       }
       acc *= 1.0f / den;
       lse_v = m + __builtin_amdgcn_logf(den) * kLn2;

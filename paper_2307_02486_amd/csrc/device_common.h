@@ -15,6 +15,7 @@ namespace {
 typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
 typedef float f32x16 __attribute__((ext_vector_type(16)));
 typedef float f32x4 __attribute__((ext_vector_type(4)));
+typedef float f32x2 __attribute__((ext_vector_type(2)));
 typedef _Float16 f16x4 __attribute__((ext_vector_type(4)));
 typedef _Float16 f16x8 __attribute__((ext_vector_type(8)));
 typedef float f32x8 __attribute__((ext_vector_type(8)));
@@ -28,7 +29,7 @@ constexpr float kLog2e = 1.442695040888963407f;
 struct PatArgs {
   int32_t w, r, nseg, lmax, ntiles, units;
   int64_t o_off;    // byte offset of this pattern's output rows in the workspace
-  int64_t lse_off;  // byte offset of this pattern's lse in the workspace
+  int64_t lse_off;  // byte offset of this pattern's (lse, scale) row records
 };
 
 // One attention work item: which segment of which pattern, and which query tile.

@@ -9,14 +9,13 @@ namespace da {
 
 // A pattern as the combine step sees it: the divisions that map a sequence
 // position to the pattern's segment and kept-row index, and where the
-// pattern's rows sit in the workspace.  Shared by the combine kernel and the
-// combine fused into the attention kernel.
+// pattern's rows sit in the workspace.
 struct MixPat {
   FastDiv fw;       // division by w
   FastDiv fr;       // division by r
   int32_t nseg, lmax;
   int64_t o_off;    // byte offset of the pattern's output rows
-  int64_t lse_off;  // byte offset of the pattern's lse
+  int64_t lse_off;  // byte offset of the pattern's (lse, scale) row records
 };
 
 inline MixPat make_mixpat(const PatternPlan& pp) {
@@ -25,23 +24,12 @@ inline MixPat make_mixpat(const PatternPlan& pp) {
                 static_cast<int64_t>(pp.o_off), static_cast<int64_t>(pp.lse_off)};
 }
 
-// Which patterns an attention launch covers.
-enum AttnPart {
-  kAllPatterns = 0,   // every pattern; the combine runs as a separate stage
-  kOtherPatterns = 1, // every pattern but plan.fuse
-  kFusedPattern = 2,  // plan.fuse only, with the combine in its epilogue
-};
-
 // Stage 1: per pattern, gather the kept rows of every segment and run causal
 // (or full) softmax attention on them, writing the normalised per-pattern
-// output and its log-sum-exp to the workspace (Sec. 2.2, Eqs. 3-6).
-// With part == kFusedPattern the launch also mixes every row of the
-// sequence (the fused pattern keeps them all) with the other patterns' rows,
-// which an earlier kOtherPatterns launch on the same stream wrote, and writes
-// out and lse (Sec. 2.2, Eqs. 7-10).
-hipError_t launch_attention(const Plan& plan, AttnPart part, const void* q, const void* k,
-                            const void* v, void* workspace, void* out, float* lse,
-                            hipStream_t stream);
+// output rows and their (lse, scale) records to the workspace
+// (Sec. 2.2, Eqs. 3-6).
+hipError_t launch_attention(const Plan& plan, const void* q, const void* k, const void* v,
+                            void* workspace, hipStream_t stream);
 
 // Stage 2: scatter the per-pattern rows back to their sequence positions and
 // mix them by their softmax denominators, writing out and lse

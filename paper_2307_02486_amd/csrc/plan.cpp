@@ -2,7 +2,6 @@
 #include "plan.h"
 
 #include <cmath>
-#include <cstdlib>
 #include <cstring>
 
 namespace da {
@@ -62,10 +61,12 @@ int make_plan(int64_t B, int64_t N, int64_t H, int64_t D, const da_pattern_t* pa
   p.npat = static_cast<int>(num_patterns);
   p.block_m = block_m_for(p.dtype);
   const int64_t esize = dtype == DA_BF16 ? 2 : 4;
-  // Per-pattern outputs are kept as fp16 for bf16 inputs (they are convex
-  // combinations of v rows, well inside fp16 range, with 3 more mantissa bits
-  // than bf16) and as fp32 for fp32 inputs.
+  // Per-pattern output rows are kept as fp16 for bf16 inputs, each row divided
+  // by a power of two that brings its largest magnitude into [2^14, 2^15)
+  // (fp16's eleven significant bits with bf16's exponent range), and as fp32
+  // for fp32 inputs.  Each row has an 8-byte record: its lse and its scale.
   const int64_t ws_esize = dtype == DA_BF16 ? 2 : 4;
+  constexpr int64_t kRecBytes = 8;
 
   uint64_t ws = 0;
   int64_t items = 0;
@@ -87,7 +88,7 @@ int make_plan(int64_t B, int64_t N, int64_t H, int64_t D, const da_pattern_t* pa
     pp.o_off = ws;
     ws = align_up(ws + rows * static_cast<uint64_t>(D) * ws_esize);
     pp.lse_off = ws;
-    ws = align_up(ws + rows * 4);
+    ws = align_up(ws + rows * kRecBytes);
 
     // exact kept rows and unmasked pairs: full segments, then the short tail
     const int64_t nfull = N / pp.w;
@@ -116,24 +117,12 @@ int make_plan(int64_t B, int64_t N, int64_t H, int64_t D, const da_pattern_t* pa
     if (static_cast<double>(p.pat[i].r) * H * D * esize * 129.0 >= 2147483648.0) p.offsets32 = false;
   // the combine stage launches one workgroup per 8..32 positions of each (b, h)
   if ((N + 7) / 8 * B * H >= (int64_t{1} << 31)) return DA_EINVAL;
-  // The combine can run inside the attention launch of an r = 1 pattern
-  // (see Plan::fuse).  Measured with a warmed-up GPU, calls alternating
-  // between the two paths in one process: 1 % slower than the separate
-  // combine at 32K tokens and equal at 256K (D = 64) although it moves 19 %
-  // fewer HBM bytes, 8 % slower at 8K tokens (B = 2).  It is therefore
-  // opt-in: DILATED_ATTN_FUSE_COMBINE=1 in the environment fuses whenever the
-  // call allows it (bf16, D <= 64, a pattern with r = 1).
-  p.fuse = -1;
-  const char* fz = std::getenv("DILATED_ATTN_FUSE_COMBINE");
-  if (fz && fz[0] == '1' && p.dtype == DA_BF16 && D <= 64)
-    for (int i = 0; i < p.npat && p.fuse < 0; ++i)
-      if (p.pat[i].r == 1) p.fuse = i;
   p.total_items = items;
   p.workspace_bytes = ws;
   p.covered_rows = covered;
   p.sparse_flops = static_cast<double>(4.0L * D * pairs);
-  p.bytes_attn = static_cast<double>(covered) * (3.0 * D * esize + D * ws_esize + 4.0);
-  p.bytes_combine = static_cast<double>(covered) * (D * ws_esize + 4.0) +
+  p.bytes_attn = static_cast<double>(covered) * (3.0 * D * esize + D * ws_esize + kRecBytes);
+  p.bytes_combine = static_cast<double>(covered) * (D * ws_esize + kRecBytes) +
                     static_cast<double>(B) * N * H * (D * esize + 4.0);
   *out = p;
   return DA_OK;

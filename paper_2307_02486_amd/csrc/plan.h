@@ -42,8 +42,10 @@ struct PatternPlan {
   int64_t units;      // B * H * nseg
   int64_t item_begin; // index of this pattern's first work item
   uint64_t o_off;     // byte offset of the per-pattern output in the workspace
-                      // (fp16 rows for bf16 inputs, fp32 rows for fp32 inputs)
-  uint64_t lse_off;   // byte offset of the per-pattern lse in the workspace
+                      // (fp16 rows scaled by a power of two for bf16 inputs,
+                      // fp32 rows for fp32 inputs)
+  uint64_t lse_off;   // byte offset of the per-row records (float lse, float
+                      // scale: the row's values are the stored ones times it)
 };
 
 struct Plan {
@@ -57,11 +59,6 @@ struct Plan {
   int64_t total_items;
   int64_t launch_items;  // workgroups of the attention launch (XCD-balanced, >= total_items)
   bool offsets32;        // every key tile spans < 2^31 bytes: 32-bit buffer offsets suffice
-  // Index of the pattern whose attention launch also runs the combine (the
-  // first pattern with r = 1, which keeps every row), or -1: the combine is
-  // a separate stage.  Fusing is opt-in (DILATED_ATTN_FUSE_COMBINE=1 in the
-  // environment) and needs bf16 inputs and D <= 64.
-  int fuse;
   uint64_t workspace_bytes;
   int64_t covered_rows;
   double sparse_flops;

@@ -9,6 +9,7 @@ libdilated_attn.so.
 from __future__ import annotations
 
 import ctypes
+import functools
 from typing import Sequence, Tuple
 
 import torch
@@ -24,17 +25,34 @@ def _dtype_code(dtype) -> int:
     return _DTYPES[dtype]
 
 
-def plan(B: int, N: int, H: int, D: int, patterns: Sequence[Tuple[int, int]], causal: bool = True,
-         dtype=torch.bfloat16, scale: float | None = None) -> dict:
-    """Validate a problem and return its workspace size and work counts (host only)."""
+def _pattern_key(patterns) -> tuple:
+    return tuple((int(w), int(r)) for (w, r) in patterns)
+
+
+@functools.lru_cache(maxsize=256)
+def _plan_cached(entry: str, B: int, N: int, H: int, D: int, pats: tuple, causal: int, dtype_code: int,
+                 scale: float):
+    """One dilated_attn_plan (or _bwd_plan) call per distinct problem: the
+    returned dict is shared, callers must not modify it."""
     lib = _lib.load()
-    arr, n = _lib.pattern_array(patterns)
+    arr, n = _lib.pattern_array(pats)
     info = _lib.PlanInfo()
-    rc = lib.dilated_attn_plan(B, N, H, D, arr, n, int(bool(causal)), _dtype_code(dtype),
-                               float(scale or 0.0), ctypes.byref(info))
+    rc = getattr(lib, entry)(B, N, H, D, arr, n, causal, dtype_code, scale, ctypes.byref(info))
     if rc != 0:
         raise _lib.DilatedAttnError(rc, lib)
     return {k: getattr(info, k) for k, _ in _lib.PlanInfo._fields_}
+
+
+@functools.lru_cache(maxsize=256)
+def _pattern_array_cached(pats: tuple):
+    return _lib.pattern_array(pats)
+
+
+def plan(B: int, N: int, H: int, D: int, patterns: Sequence[Tuple[int, int]], causal: bool = True,
+         dtype=torch.bfloat16, scale: float | None = None) -> dict:
+    """Validate a problem and return its workspace size and work counts (host only)."""
+    return dict(_plan_cached("dilated_attn_plan", int(B), int(N), int(H), int(D), _pattern_key(patterns),
+                             int(bool(causal)), _dtype_code(dtype), float(scale or 0.0)))
 
 
 def plan_raw(B, N, H, D, patterns, causal, dtype_code, scale):
@@ -49,8 +67,23 @@ def plan_raw(B, N, H, D, patterns, causal, dtype_code, scale):
 def workspace_for(q: torch.Tensor, patterns, causal=True, scale=None) -> torch.Tensor:
     """Allocate (with torch) the device workspace a call on q's shape needs."""
     B, N, H, D = q.shape
-    info = plan(B, N, H, D, patterns, causal, q.dtype, scale)
+    info = _plan_cached("dilated_attn_plan", B, N, H, D, _pattern_key(patterns), int(bool(causal)),
+                        _dtype_code(q.dtype), float(scale or 0.0))
     return torch.empty(max(256, int(info["workspace_bytes"])), dtype=torch.uint8, device=q.device)
+
+
+def _check_like(name: str, t: torch.Tensor, shape, dtype, device):
+    if t.shape != tuple(shape) or t.dtype != dtype or t.device != device or not t.is_contiguous():
+        raise ValueError(f"{name} must be a contiguous {dtype} tensor of shape {tuple(shape)} on {device}")
+
+
+def _stream_use(stream, owned):
+    """Tensors this binding allocated on torch's current stream but handed to
+    another stream's kernels: tell the allocator, so that their memory is not
+    reused before that stream's work is done."""
+    if stream != torch.cuda.current_stream(stream.device):
+        for t in owned:
+            t.record_stream(stream)
 
 
 def dilated_attn(q: torch.Tensor, k: torch.Tensor, v: torch.Tensor,
@@ -62,41 +95,55 @@ def dilated_attn(q: torch.Tensor, k: torch.Tensor, v: torch.Tensor,
 
     Returns (out [B,N,H,D] in q's dtype, lse [B,H,N] float32).  Work is
     enqueued on `stream` (default: torch's current stream) and not waited for.
+    A given out, lse or workspace must be a contiguous tensor of the right
+    shape, dtype and device (workspace: uint8, at least the planned size).
     """
     lib = _lib.load()
     if q.device.type != "cuda":
         raise RuntimeError("dilated_attn runs on the GPU only; q must be a device tensor")
+    if q.dim() != 4:
+        raise ValueError("q, k, v must be [B, N, H, D]")
     for t in (q, k, v):
         if not t.is_contiguous() or t.shape != q.shape or t.dtype != q.dtype or t.device != q.device:
             raise ValueError("q, k, v must be contiguous tensors of the same shape, dtype and device")
-    if q.dim() != 4:
-        raise ValueError("q, k, v must be [B, N, H, D]")
     B, N, H, D = q.shape
+    pats = _pattern_key(patterns)
+    dcode = _dtype_code(q.dtype)
+    sc = float(scale or 0.0)
+    info = _plan_cached("dilated_attn_plan", B, N, H, D, pats, int(bool(causal)), dcode, sc)
+    owned = []
     if out is None:
         out = torch.empty_like(q)
+        owned.append(out)
+    else:
+        _check_like("out", out, q.shape, q.dtype, q.device)
     if lse is None:
         lse = torch.empty((B, H, N), dtype=torch.float32, device=q.device)
+        owned.append(lse)
+    else:
+        _check_like("lse", lse, (B, H, N), torch.float32, q.device)
     if workspace is None:
-        workspace = workspace_for(q, patterns, causal, scale)
+        workspace = torch.empty(max(256, int(info["workspace_bytes"])), dtype=torch.uint8, device=q.device)
+        owned.append(workspace)
+    elif workspace.dtype != torch.uint8 or workspace.device != q.device or not workspace.is_contiguous():
+        raise ValueError("workspace must be a contiguous uint8 tensor on q's device")
     if stream is None:
         stream = torch.cuda.current_stream(q.device)
-    arr, n = _lib.pattern_array(patterns)
+    arr, n = _pattern_array_cached(pats)
     rc = lib.dilated_attn_fwd(q.data_ptr(), k.data_ptr(), v.data_ptr(), out.data_ptr(), lse.data_ptr(),
-                              B, N, H, D, arr, n, int(bool(causal)), _dtype_code(q.dtype),
-                              float(scale or 0.0), workspace.data_ptr(), workspace.numel(),
-                              stream.cuda_stream)
+                              B, N, H, D, arr, n, int(bool(causal)), dcode, sc,
+                              workspace.data_ptr(), workspace.numel(), stream.cuda_stream)
     if rc != 0:
         raise _lib.DilatedAttnError(rc, lib)
+    _stream_use(stream, owned)
     return out, lse
 
 
 class StageTimer:
     """Context manager around dilated_attn_profile_begin/end: HIP event timing
     of the two launches of each call made inside it (on the call's own
-    stream).  ms_attention and ms_combine sum the first and second launch:
-    the attention and the combine stage, or, with the combine fused
-    (plan(...)["combine_fused"]), the attention launch of the patterns other
-    than the fused one and the fused pattern's launch with the combine."""
+    stream).  ms_attention and ms_combine sum the attention and the combine
+    stage."""
 
     def __init__(self, capacity: int = 4096):
         self.capacity = capacity
@@ -123,14 +170,8 @@ class StageTimer:
 def plan_bwd(B: int, N: int, H: int, D: int, patterns: Sequence[Tuple[int, int]], causal: bool = True,
              dtype=torch.bfloat16, scale: float | None = None) -> dict:
     """Validate a backward problem and return its workspace size and work (host only)."""
-    lib = _lib.load()
-    arr, n = _lib.pattern_array(patterns)
-    info = _lib.PlanInfo()
-    rc = lib.dilated_attn_bwd_plan(B, N, H, D, arr, n, int(bool(causal)), _dtype_code(dtype),
-                                   float(scale or 0.0), ctypes.byref(info))
-    if rc != 0:
-        raise _lib.DilatedAttnError(rc, lib)
-    return {k: getattr(info, k) for k, _ in _lib.PlanInfo._fields_}
+    return dict(_plan_cached("dilated_attn_bwd_plan", int(B), int(N), int(H), int(D), _pattern_key(patterns),
+                             int(bool(causal)), _dtype_code(dtype), float(scale or 0.0)))
 
 
 def bwd_workspace_for(q: torch.Tensor, patterns, causal=True, scale=None) -> torch.Tensor:
@@ -147,32 +188,48 @@ def dilated_attn_bwd(q: torch.Tensor, k: torch.Tensor, v: torch.Tensor, out: tor
                      workspace: torch.Tensor | None = None, stream: torch.cuda.Stream | None = None):
     """Dilated-attention backward: (dq, dk, dv) given the forward's inputs and
     outputs (out, lse) and dout, all on the GPU, [B, N, H, D] contiguous
-    (lse [B, H, N] float32).  Enqueued on `stream` and not waited for."""
+    (lse [B, H, N] float32).  Enqueued on `stream` and not waited for.  A
+    given dq, dk, dv or workspace must be a contiguous tensor of the right
+    shape, dtype and device."""
     lib = _lib.load()
     if q.device.type != "cuda":
         raise RuntimeError("dilated_attn_bwd runs on the GPU only; q must be a device tensor")
+    if q.dim() != 4:
+        raise ValueError("tensors must be [B, N, H, D]")
     for t in (q, k, v, out, dout):
         if not t.is_contiguous() or t.shape != q.shape or t.dtype != q.dtype or t.device != q.device:
             raise ValueError("q, k, v, out, dout must be contiguous tensors of the same shape, dtype, device")
-    if q.dim() != 4:
-        raise ValueError("tensors must be [B, N, H, D]")
     B, N, H, D = q.shape
-    if lse.shape != (B, H, N) or lse.dtype != torch.float32 or not lse.is_contiguous():
-        raise ValueError("lse must be a contiguous float32 [B, H, N] tensor")
-    dq = torch.empty_like(q) if dq is None else dq
-    dk = torch.empty_like(q) if dk is None else dk
-    dv = torch.empty_like(q) if dv is None else dv
+    _check_like("lse", lse, (B, H, N), torch.float32, q.device)
+    pats = _pattern_key(patterns)
+    dcode = _dtype_code(q.dtype)
+    sc = float(scale or 0.0)
+    info = _plan_cached("dilated_attn_bwd_plan", B, N, H, D, pats, int(bool(causal)), dcode, sc)
+    owned = []
+    grads = []
+    for name, g in (("dq", dq), ("dk", dk), ("dv", dv)):
+        if g is None:
+            g = torch.empty_like(q)
+            owned.append(g)
+        else:
+            _check_like(name, g, q.shape, q.dtype, q.device)
+        grads.append(g)
+    dq, dk, dv = grads
     if workspace is None:
-        workspace = bwd_workspace_for(q, patterns, causal, scale)
+        workspace = torch.empty(max(256, int(info["workspace_bytes"])), dtype=torch.uint8, device=q.device)
+        owned.append(workspace)
+    elif workspace.dtype != torch.uint8 or workspace.device != q.device or not workspace.is_contiguous():
+        raise ValueError("workspace must be a contiguous uint8 tensor on q's device")
     if stream is None:
         stream = torch.cuda.current_stream(q.device)
-    arr, n = _lib.pattern_array(patterns)
+    arr, n = _pattern_array_cached(pats)
     rc = lib.dilated_attn_bwd(q.data_ptr(), k.data_ptr(), v.data_ptr(), out.data_ptr(), lse.data_ptr(),
                               dout.data_ptr(), dq.data_ptr(), dk.data_ptr(), dv.data_ptr(), B, N, H, D,
-                              arr, n, int(bool(causal)), _dtype_code(q.dtype), float(scale or 0.0),
+                              arr, n, int(bool(causal)), dcode, sc,
                               workspace.data_ptr(), workspace.numel(), stream.cuda_stream)
     if rc != 0:
         raise _lib.DilatedAttnError(rc, lib)
+    _stream_use(stream, owned)
     return dq, dk, dv
 
 

@@ -78,30 +78,36 @@ def test_plan_accounting_matches_enumeration(wl):
     assert info["covered_rows"] == rows
     assert info["sparse_flops"] == pytest.approx(flops, rel=1e-12)
     es = 2 if wl.dtype == "bf16" else 4     # element size of q, k, v, out
-    ws = 2 if wl.dtype == "bf16" else 4     # per-pattern outputs: fp16 or fp32
-    assert info["bytes_attn"] == rows * (3 * wl.D * es + wl.D * ws + 4)
-    assert info["bytes_combine"] == rows * (wl.D * ws + 4) + wl.B * wl.N * wl.H * (wl.D * es + 4)
+    ws = 2 if wl.dtype == "bf16" else 4     # per-pattern outputs: scaled fp16 or fp32
+    rec = 8                                 # per-row record: lse and scale (float32 each)
+    assert info["bytes_attn"] == rows * (3 * wl.D * es + wl.D * ws + rec)
+    assert info["bytes_combine"] == rows * (wl.D * ws + rec) + wl.B * wl.N * wl.H * (wl.D * es + 4)
 
 
-BENCH_PATS = [(2048, 1), (4096, 2), (8192, 4), (16384, 6), (32768, 12)]
-
-
-@pytest.mark.parametrize("N,H,D,dtype,pats,env,fused", [
-    (32768, 12, 64, torch.bfloat16, BENCH_PATS, None, 0),       # separate combine by default
-    (32768, 12, 64, torch.bfloat16, BENCH_PATS, "1", 1),        # opt-in
-    (8192, 12, 32, torch.bfloat16, BENCH_PATS[::-1], "1", 1),   # the r = 1 pattern need not come first
-    (32768, 12, 64, torch.bfloat16, [(64, 3), (128, 2)], "1", 0),  # no pattern keeps every row
-    (32768, 12, 128, torch.bfloat16, BENCH_PATS, "1", 0),       # D = 128: separate combine
-    (32768, 12, 64, torch.float32, BENCH_PATS, "1", 0),         # fp32: separate combine
-    (32768, 12, 64, torch.bfloat16, BENCH_PATS, "0", 0),
-])
-def test_plan_combine_fused(N, H, D, dtype, pats, env, fused, monkeypatch):
+def test_plan_workspace_layout():
+    """Workspace per pattern: compact output rows (fp16 for bf16 inputs, fp32
+    for fp32 inputs) and an 8-byte record per row, each block 256-byte aligned."""
     from paper_2307_02486_amd import plan
-    if env is None:
-        monkeypatch.delenv("DILATED_ATTN_FUSE_COMBINE", raising=False)
-    else:
-        monkeypatch.setenv("DILATED_ATTN_FUSE_COMBINE", env)
-    assert plan(1, N, H, D, pats, True, dtype)["combine_fused"] == fused
+    pats = [(2048, 1), (4096, 2), (8192, 4), (16384, 6), (32768, 12)]
+    for dtype, es in ((torch.bfloat16, 2), (torch.float32, 4)):
+        info = plan(1, 32768, 12, 64, pats, True, dtype)
+        want = 0
+        for (w, r) in pats:
+            rows = 12 * (32768 // w) * (-(-w // r))
+            want += -(-rows * 64 * es // 256) * 256
+            want += -(-rows * 8 // 256) * 256
+        assert info["workspace_bytes"] == want
+
+
+def test_plan_takes_no_environment_switch(monkeypatch):
+    """What a call computes and launches depends on its arguments only."""
+    from paper_2307_02486_amd.ops import plan_raw
+    pats = [(2048, 1), (4096, 2)]
+    rc0, i0 = plan_raw(1, 8192, 12, 64, pats, 1, 1, 0.0)
+    monkeypatch.setenv("DILATED_ATTN_FUSE_COMBINE", "1")
+    rc1, i1 = plan_raw(1, 8192, 12, 64, pats, 1, 1, 0.0)
+    assert rc0 == rc1 == 0 and i0 == i1
+    assert "combine_fused" not in i0
 
 
 def test_plan_accounting_random_small():
