@@ -8,8 +8,11 @@
 // the offsets of Sec. 2.3):
 //   P = exp(scale q.k - lse),  dS = P (dout.v - delta),
 //   dq += scale dS k,  dk += scale dS q,  dv += P dout.
+// Scores are exact bf16 products q.k summed in fp32; the softmax scale is
+// applied to the fp32 sum (P = exp2(scale log2(e) (q.k - lse / scale))), so q
+// and k enter the MFMAs as given.
 // Four kernels:
-//   bwd_delta  per row: -delta and -lse*log2(e) into the workspace;
+//   bwd_delta  per row: -delta and -lse/scale into the workspace;
 //   bwd_dq     per (pattern, segment, 128-query tile): each lane owns a query;
 //              over the segment's key tiles, S^T = K Q^T and (dP - delta)^T =
 //              V dO^T start from -lse and -delta (no running max: lse is
@@ -42,7 +45,7 @@ struct BwdArgs {
   const void* k;
   const void* v;
   const void* dout;
-  const float* nl2;  // -lse * log2(e), [B][H][N]
+  const float* nl2;  // -lse / scale, [B][H][N]: the score offset before the scale
   const float* nd;   // -delta, [B][H][N]
   char* ws;
   int32_t B, N, H, npat, causal;
@@ -129,7 +132,7 @@ struct TileLoader {
 };
 
 // ---------------------------------------------------------------------------
-// bwd_delta: -delta = -sum_d dout*out and -lse*log2(e), per (b, h, p).
+// bwd_delta: -delta = -sum_d dout*out and -lse/scale, per (b, h, p).
 // ---------------------------------------------------------------------------
 struct DeltaArgs {
   const u16* out;
@@ -137,6 +140,7 @@ struct DeltaArgs {
   const float* lse;
   float* nl2;
   float* nd;
+  float inv_scale;
   int32_t N, H, chunks;
 };
 
@@ -168,7 +172,7 @@ __global__ __launch_bounds__(kThreadsB) void bwd_delta(DeltaArgs a) {
   if (ok && d0 == 0) {
     const int64_t o2 = (int64_t)bh * a.N + p;
     a.nd[o2] = -acc;
-    a.nl2[o2] = -a.lse[o2] * kLog2e;
+    a.nl2[o2] = -a.lse[o2] * a.inv_scale;
   }
 }
 
@@ -216,7 +220,7 @@ __global__ __launch_bounds__(kThreadsB) void bwd_dq(BwdArgs a) {
   // -lse*log2e and -delta.
   const int64_t qoff = (it.row0 + (int64_t)qrow * it.rstride) * D;
   bf16x8 qreg[KC], doreg[KC];
-  load_rowslices<KC>(static_cast<const u16*>(a.q) + qoff, hi, a.scale_log2, !q_valid, qreg);
+  load_rowslices<KC>(static_cast<const u16*>(a.q) + qoff, hi, 1.0f, !q_valid, qreg);
   load_rowslices<KC>(static_cast<const u16*>(a.dout) + qoff, hi, 1.0f, !q_valid, doreg);
   const int64_t srow = ((int64_t)it.b * a.H + it.h) * a.N + it.p0 + (int64_t)qrow * P.r;
   const float nl2 = a.nl2[srow], nd = a.nd[srow];
@@ -257,7 +261,7 @@ __global__ __launch_bounds__(kThreadsB) void bwd_dq(BwdArgs a) {
       const uint32_t kaddr = lds_addr(kl);
       static_for<0, SB>([&](auto KB) {
         constexpr int kb = decltype(KB)::value;
-        // S'^T = K Q'^T - lse*log2e and (dP - delta)^T = V dO^T - delta
+        // S'^T = K Q^T - lse/scale and (dP - delta)^T = V dO^T - delta
         u32x4 kf[KC], vf[KC];
 #pragma unroll
         for (int c = 0; c < KC; ++c) {
@@ -281,7 +285,8 @@ __global__ __launch_bounds__(kThreadsB) void bwd_dq(BwdArgs a) {
 #pragma unroll
         for (int kk = 0; kk < 2; ++kk)
 #pragma unroll
-          for (int e = 0; e < 8; ++e) dsb[kk][e] = (__bf16)(__builtin_amdgcn_exp2f(s[8 * kk + e]) * dp[8 * kk + e]);
+          for (int e = 0; e < 8; ++e)
+            dsb[kk][e] = (__bf16)(__builtin_amdgcn_exp2f(s[8 * kk + e] * a.scale_log2) * dp[8 * kk + e]);
         // K^T fragments through transposed reads (keys kb*32 + 16kk + 8t + 4hi + {0..3})
         u32x2 kt[2][DB][2];
         static_for<0, 2>([&](auto KK) {
@@ -376,10 +381,10 @@ __global__ __launch_bounds__(kThreadsB) void bwd_dkdv(BwdArgs a) {
   };
   if (qt_first < qt_end) load_tile(qt_first, 0);
 
-  // K^T (times scale*log2e) and V^T operands of this lane's key.
+  // K^T and V^T operands of this lane's key (as given).
   const int64_t koff = (it.row0 + (int64_t)krow * it.rstride) * D;
   bf16x8 kreg[KC], vreg[KC];
-  load_rowslices<KC>(static_cast<const u16*>(a.k) + koff, hi, a.scale_log2, !k_valid, kreg);
+  load_rowslices<KC>(static_cast<const u16*>(a.k) + koff, hi, 1.0f, !k_valid, kreg);
   load_rowslices<KC>(static_cast<const u16*>(a.v) + koff, hi, 1.0f, !k_valid, vreg);
   f32x16 acc_dk[DB], acc_dv[DB];
 #pragma unroll
@@ -448,7 +453,7 @@ __global__ __launch_bounds__(kThreadsB) void bwd_dkdv(BwdArgs a) {
         for (int kk = 0; kk < 2; ++kk)
 #pragma unroll
           for (int e = 0; e < 8; ++e) {
-            const float p = __builtin_amdgcn_exp2f(s[8 * kk + e]);
+            const float p = __builtin_amdgcn_exp2f(s[8 * kk + e] * a.scale_log2);
             pb[kk][e] = (__bf16)p;
             dsb[kk][e] = (__bf16)(p * dp[8 * kk + e]);
           }
@@ -583,6 +588,7 @@ hipError_t launch_backward(const Plan& plan, const BwdLayout& lay, const void* q
   da_.lse = lse;
   da_.nl2 = reinterpret_cast<float*>(ws + lay.nl2_off);
   da_.nd = reinterpret_cast<float*>(ws + lay.nd_off);
+  da_.inv_scale = 1.0f / plan.scale;
   da_.N = static_cast<int32_t>(plan.N);
   da_.H = static_cast<int32_t>(plan.H);
   da_.chunks = chunks;

@@ -252,7 +252,11 @@ __global__ __launch_bounds__(kThreads) void attn_fwd_bf16(AttnArgs a) {
       }
       // Mask keys after the query (causal) and past the segment's end.
       if ((a.causal && k0 + BN - 1 > wq_lo) || k0 + BN > L) {
-        const int base = k0 + 4 * hi - lim;   // key - lim = base + offset(kb, j)
+        int base = k0 + 4 * hi - lim;   // key - lim = base + offset(kb, j)
+        // Opaque to the compiler, so that the compares are made here: hoisted
+        // out of the loops (for the first tile) they become 32 lane masks held
+        // in scalar registers, which spill.
+        asm volatile("" : "+v"(base));
 #pragma unroll
         for (int kb = 0; kb < SB; ++kb)
 #pragma unroll

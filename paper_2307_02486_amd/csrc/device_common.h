@@ -198,9 +198,11 @@ __device__ inline u32x2 lds_read_tr16(uint32_t addr) {
   asm volatile("ds_read_b64_tr_b16 %0, %1 offset:%2" : "=v"(r) : "v"(addr), "i"(kOff) : "memory");
   return r;
 }
+// The counter field holds at most 15: a wave cannot have more LDS operations
+// in flight, so with more than 15 younger ones issued the awaited one is done.
 template <int N>
 __device__ inline void lds_wait() {
-  asm volatile("s_waitcnt lgkmcnt(%0)" ::"i"(N) : "memory");
+  asm volatile("s_waitcnt lgkmcnt(%0)" ::"i"(N > 15 ? 15 : N) : "memory");
 }
 __device__ inline void lds_bind(u32x2& r) { asm volatile("" : "+v"(r)); }
 

@@ -155,3 +155,30 @@ def test_backward_n1m_sampled_rows():
     for n, g, r in (("dk", dk, rk), ("dv", dv, rv)):
         e = _check(n, pick(g.cpu(), krows), r, "n1m")
         note(f"[bwd] n1m {n}: {len(krows)} rows, err {e:.2e}")
+
+
+@pytest.mark.parametrize("scale_kind", ["default", "generic"])
+def test_backward_large_scores(scale_kind):
+    """Scores four times the workloads' (q, k ~ N(0, 2^2)) with the default
+    scale at the 8K workload's shapes (every row of heads 0 and 5), and with a
+    scale whose product with log2(e) is not a short binary fraction on a
+    smaller ragged case: q and k enter the score MFMAs unrounded."""
+    if scale_kind == "default":
+        wl = workloads.BY_NAME["n8k_b2_h12_d64_3pat"]
+        shape, pats, hs, scale = (wl.B, wl.N, wl.H, wl.D), list(wl.patterns), [0, 5], None
+    else:
+        shape, pats, hs, scale = (1, 777, 3, 64), [(256, 1), (512, 7), (777, 3)], None, 0.1301 / 1.4426950408889634
+    note(f"[bwd] large scores {scale_kind} {shape}")
+    q = workloads.make_random(shape, torch.bfloat16, 2.0, 4343, "cuda", 0)
+    k = workloads.make_random(shape, torch.bfloat16, 2.0, 4343, "cuda", 1)
+    v = workloads.make_random(shape, torch.bfloat16, 1.0, 4343, "cuda", 2)
+    dout = workloads.make_random(shape, torch.bfloat16, 1.0, 4343, "cuda", 3)
+    dq, dk, dv = _gpu_bwd(q, k, v, dout, pats, True, scale)
+    rq, rk, rv, _, _ = oracle.dilated_attention_bwd_ref(to64(q), to64(k), to64(v), to64(dout), pats, True,
+                                                        scale, heads=hs)
+    for n, g, r in (("dq", dq, rq), ("dk", dk, rk), ("dv", dv, rv)):
+        gg, rr = to64(g), r
+        if hs is not None:
+            gg, rr = gg[:, :, hs], rr[:, :, hs]
+        e = _check(n, gg, rr, f"large scores {scale_kind}")
+        note(f"[bwd] large scores {scale_kind} {n} err {e:.2e}")
