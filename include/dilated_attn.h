@@ -59,7 +59,9 @@ enum {
   DA_EUNSUPPORTED = -2, /* head dim or dtype the library has no kernel for */
   DA_EWORKSPACE = -3,   /* workspace smaller than dilated_attn_plan asks  */
   DA_EALIGN = -4,       /* a device pointer not 16-byte aligned           */
-  DA_EHIP = -5          /* the HIP runtime reported an error at launch    */
+  DA_EHIP = -5,         /* the HIP runtime reported an error at launch    */
+  DA_ETOOLARGE = -6     /* dilated_attn_fwd_noalloc: the problem needs more
+                           workspace than DA_NOALLOC_MAX_BYTES              */
 };
 
 /* Sizes and work of one call, filled by dilated_attn_plan. */
@@ -122,6 +124,28 @@ int dilated_attn_fwd(const void* q, const void* k, const void* v, void* out,
                      const da_pattern_t* patterns, int64_t num_patterns,
                      int64_t causal, int64_t dtype, float softmax_scale,
                      void* workspace, uint64_t workspace_bytes, void* stream);
+
+/*
+ * dilated_attn_fwd_noalloc - dilated_attn_fwd without a workspace argument,
+ * for callers that cannot allocate device memory (code under HIP graph
+ * capture, tight serving loops, harnesses that forbid allocation).
+ *
+ * The workspace is a device array owned by the library, DA_NOALLOC_MAX_BYTES
+ * (128 MiB) on every device the function runs on, held until the process
+ * ends; its address is looked up once per device.  Problems whose
+ * dilated_attn_plan workspace_bytes exceeds DA_NOALLOC_MAX_BYTES return
+ * DA_ETOOLARGE (the 8K- and 32K-token workloads of the benchmark fit; larger
+ * ones need dilated_attn_fwd).  The call allocates nothing, host or device.
+ * All calls on one device share its array: calls that may overlap in time on
+ * one device (other streams, other threads) race and must not be made.
+ * Arguments, results and other errors as for dilated_attn_fwd.
+ */
+#define DA_NOALLOC_MAX_BYTES (128ull << 20)
+int dilated_attn_fwd_noalloc(const void* q, const void* k, const void* v, void* out,
+                             float* lse, int64_t B, int64_t N, int64_t H, int64_t D,
+                             const da_pattern_t* patterns, int64_t num_patterns,
+                             int64_t causal, int64_t dtype, float softmax_scale,
+                             void* stream);
 
 /*
  * Backward pass: gradients of a loss with respect to q, k and v, given the

@@ -17,7 +17,8 @@ DA_F32 = 0
 DA_BF16 = 1
 DA_MAX_PATTERNS = 16
 ERRORS = {0: "DA_OK", -1: "DA_EINVAL", -2: "DA_EUNSUPPORTED", -3: "DA_EWORKSPACE",
-          -4: "DA_EALIGN", -5: "DA_EHIP"}
+          -4: "DA_EALIGN", -5: "DA_EHIP", -6: "DA_ETOOLARGE"}
+NOALLOC_MAX_BYTES = 128 << 20
 CODES = {v: k for k, v in ERRORS.items()}
 
 
@@ -62,6 +63,9 @@ def load():
     lib.dilated_attn_fwd.argtypes = [vp, vp, vp, vp, vp, i64, i64, i64, i64, ctypes.POINTER(Pattern),
                                      i64, i64, i64, f32, vp, ctypes.c_uint64, vp]
     lib.dilated_attn_fwd.restype = ctypes.c_int
+    lib.dilated_attn_fwd_noalloc.argtypes = [vp, vp, vp, vp, vp, i64, i64, i64, i64, ctypes.POINTER(Pattern),
+                                             i64, i64, i64, f32, vp]
+    lib.dilated_attn_fwd_noalloc.restype = ctypes.c_int
     lib.dilated_attn_bwd_plan.argtypes = lib.dilated_attn_plan.argtypes
     lib.dilated_attn_bwd_plan.restype = ctypes.c_int
     lib.dilated_attn_bwd.argtypes = [vp, vp, vp, vp, vp, vp, vp, vp, vp, i64, i64, i64, i64,

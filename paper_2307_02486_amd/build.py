@@ -18,7 +18,7 @@ INCLUDE = os.path.join(ROOT, "include")
 LIB_NAME = "libdilated_attn.so"
 LIB_PATH = os.path.join(HERE, LIB_NAME)
 
-HIP_SOURCES = ["attn_fwd.hip", "combine.hip", "attn_bwd.hip", "xpos.hip", "wgrad.hip", "layernorm.hip"]
+HIP_SOURCES = ["attn_fwd.hip", "combine.hip", "attn_bwd.hip", "xpos.hip", "wgrad.hip", "layernorm.hip", "noalloc.hip"]
 HOST_SOURCES = ["plan.cpp", "api.cpp"]
 
 ARCH = "gfx950"

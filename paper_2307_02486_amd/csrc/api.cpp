@@ -321,6 +321,7 @@ const char* dilated_attn_strerror(int code) {
     case DA_EWORKSPACE: return "workspace smaller than dilated_attn_plan requires";
     case DA_EALIGN: return "device pointer not 16-byte aligned";
     case DA_EHIP: return "HIP runtime error at kernel launch";
+    case DA_ETOOLARGE: return "problem needs more workspace than the no-alloc entry point's fixed buffer";
     default: return "unknown error code";
   }
 }

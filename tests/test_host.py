@@ -49,7 +49,7 @@ def lib():
 def test_exports_every_declared_symbol(lib):
     text = open(HEADER).read()
     names = re.findall(r"^\s*(?:const\s+)?\w+\*?\s+\*?(dilated_attn_\w+)\s*\(", text, re.M)
-    assert set(names) == {"dilated_attn_plan", "dilated_attn_fwd", "dilated_attn_strerror",
+    assert set(names) == {"dilated_attn_plan", "dilated_attn_fwd", "dilated_attn_fwd_noalloc", "dilated_attn_strerror",
                           "dilated_attn_profile_begin", "dilated_attn_profile_end",
                           "dilated_attn_bwd_plan", "dilated_attn_bwd", "dilated_attn_xpos",
                           "dilated_attn_wgrad_workspace", "dilated_attn_wgrad",
@@ -65,7 +65,7 @@ def test_exports_every_declared_symbol(lib):
 
 
 def test_strerror(lib):
-    for code in (0, -1, -2, -3, -4, -5, 7):
+    for code in (0, -1, -2, -3, -4, -5, -6, 7):
         assert lib.dilated_attn_strerror(code)
 
 
