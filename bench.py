@@ -490,6 +490,18 @@ def main():
                      "traffic": prof.get("attention_bytes_per_launch")},
         "cpu_baseline": None,
     }
+    # Host side of one call (Python binding, ctypes, plan, two launches): the
+    # GPU is kept busy by a queue of calls, so enqueueing never waits on it.
+    warm()
+    for _ in range(20):
+        step()
+    n_host = 100
+    t0 = time.perf_counter()
+    for _ in range(n_host):
+        step()
+    host_us = (time.perf_counter() - t0) / n_host * 1e6
+    torch.cuda.synchronize()
+    res["host_us_per_call"] = round(host_us, 2)
     if args.dist_steps > 0:
         warm()
         res["step_distribution"] = {
@@ -549,13 +561,18 @@ def large_workload(wl, args):
     flops = info["sparse_flops"]
     attn_tflops = flops / (ms_attn * 1e-3) / 1e12
     comb_gbs = info["bytes_combine"] / (ms_comb * 1e-3) / 1e9
+    prof = profiled_counters(wl.name)
     rec = {"config": wl.describe(), "calls": calls, "ms_per_call": round(ms, 4),
            "tflops": round(flops / (ms * 1e-3) / 1e12, 3), "tokens_per_s": round(wl.B * wl.N / (ms * 1e-3), 1),
            "sparse_flops": flops, "workspace_bytes": info["workspace_bytes"],
            "attention_stage": {"ms": round(ms_attn, 4), "tflops": round(attn_tflops, 3),
-                               "frac_of_mfma_peak": round(attn_tflops / PEAK_BF16_TFLOPS, 4)},
+                               "frac_of_mfma_peak": round(attn_tflops / PEAK_BF16_TFLOPS, 4),
+                               "algorithmic_bytes": info["bytes_attn"],
+                               "traffic": prof.get("attention_bytes_per_launch"),
+                               "mfma_busy_pct_profiled": prof.get("attention_mfma_busy_pct")},
            "combine_stage": {"ms": round(ms_comb, 4), "algorithmic_bytes": info["bytes_combine"],
-                             "gbps": round(comb_gbs, 1), "frac_of_hbm_peak": round(comb_gbs / PEAK_HBM_GBS, 4)}}
+                             "gbps": round(comb_gbs, 1), "frac_of_hbm_peak": round(comb_gbs / PEAK_HBM_GBS, 4),
+                             "traffic": prof.get("combine_bytes_per_launch")}}
     del q, k, v, out, lse, ws
     torch.cuda.empty_cache()
     return rec
