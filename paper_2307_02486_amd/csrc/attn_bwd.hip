@@ -22,6 +22,9 @@
 //              dO V^T, then dV^T += dO^T P and dK^T += Q^T dS;
 //   bwd_sum    per row: the compact per-pattern gradients of every pattern
 //              that keeps the row, summed and rounded to bf16.
+// The compact per-pattern gradients are fp16 rows scaled by a power of two
+// per row and 64-column chunk (row_scale), with the float scale beside them:
+// an error of at most 2^-11 of the chunk's largest element before the sum.
 // Tiles of the rows that are shared by a workgroup (K/V for dq, Q/dO for
 // dk/dv) go from HBM into LDS without passing through registers; transposed
 // operands come from transposed LDS reads.  Work items are mapped to XCDs as
@@ -37,7 +40,8 @@ namespace {
 
 struct BwdPat {
   int32_t w, r, nseg, lmax, ntiles, units;
-  int64_t dq_off, dk_off, dv_off;  // byte offsets of the compact float32 gradients
+  int64_t dq_off, dk_off, dv_off;           // byte offsets of the compact fp16 gradient rows
+  int64_t dq_rec_off, dk_rec_off, dv_rec_off;  // and of their float scales
 };
 
 struct BwdArgs {
@@ -60,6 +64,9 @@ constexpr int kThreadsB = 256;  // four waves
 // scores and dP are recomputed, the accumulators fit in registers).
 template <int D>
 constexpr int kCols = D <= 64 ? D : 64;
+// Scales per compact gradient row: one per item's column range.
+template <int D>
+constexpr int kChunks = D / kCols<D>;
 // Launch index of a split work item: the two halves of an item take two
 // consecutive slots of the same XCD.  Returns the item's launch index and sets
 // `half`.
@@ -314,15 +321,27 @@ __global__ __launch_bounds__(kThreadsB) void bwd_dq(BwdArgs a) {
     __syncthreads();
   }
 
+  // dq = scale * acc over this item's columns, stored scaled (both half-waves
+  // hold parts of the row: the max is exchanged before any lane leaves).
+  float amax = 0.0f;
+#pragma unroll
+  for (int db = 0; db < DB; ++db)
+#pragma unroll
+    for (int j = 0; j < 16; ++j) amax = fmaxf(amax, fabsf(acc_dq[db][j]));
+  amax = fmaxf(amax, other_half(amax));
   if (!q_valid) return;
-  float* orow = reinterpret_cast<float*>(a.ws + P.dq_off) + ((int64_t)it.unit * P.lmax + tq_row) * D;
+  float mul, rs;
+  row_scale(amax * a.scale, a.scale, mul, rs);
+  const int64_t wrow = (int64_t)it.unit * P.lmax + tq_row;
+  _Float16* orow = reinterpret_cast<_Float16*>(a.ws + P.dq_off) + wrow * D;
 #pragma unroll
   for (int db = 0; db < DB; ++db)
 #pragma unroll
     for (int jj = 0; jj < 4; ++jj)
-      *reinterpret_cast<f32x4*>(orow + c0 + db * 32 + 8 * jj + 4 * hi) =
-          f32x4{acc_dq[db][4 * jj] * a.scale, acc_dq[db][4 * jj + 1] * a.scale,
-                acc_dq[db][4 * jj + 2] * a.scale, acc_dq[db][4 * jj + 3] * a.scale};
+      *reinterpret_cast<f16x4*>(orow + c0 + db * 32 + 8 * jj + 4 * hi) =
+          f16x4{(_Float16)(acc_dq[db][4 * jj] * mul), (_Float16)(acc_dq[db][4 * jj + 1] * mul),
+                (_Float16)(acc_dq[db][4 * jj + 2] * mul), (_Float16)(acc_dq[db][4 * jj + 3] * mul)};
+  if (hi == 0) reinterpret_cast<float*>(a.ws + P.dq_rec_off)[wrow * kChunks<D> + half] = rs;
 }
 
 // ---------------------------------------------------------------------------
@@ -492,21 +511,41 @@ __global__ __launch_bounds__(kThreadsB) void bwd_dkdv(BwdArgs a) {
     __syncthreads();
   }
 
+  // dk = scale * acc_dk and dv = acc_dv over this item's columns, stored
+  // scaled (the row maxima are exchanged before any lane leaves).
+  float amax_k = 0.0f, amax_v = 0.0f;
+#pragma unroll
+  for (int db = 0; db < DB; ++db)
+#pragma unroll
+    for (int j = 0; j < 16; ++j) {
+      amax_k = fmaxf(amax_k, fabsf(acc_dk[db][j]));
+      amax_v = fmaxf(amax_v, fabsf(acc_dv[db][j]));
+    }
+  amax_k = fmaxf(amax_k, other_half(amax_k));
+  amax_v = fmaxf(amax_v, other_half(amax_v));
   if (!k_valid) return;
-  const int64_t wrow = ((int64_t)it.unit * P.lmax + tk_row) * D;
-  float* krow_out = reinterpret_cast<float*>(a.ws + P.dk_off) + wrow;
-  float* vrow_out = reinterpret_cast<float*>(a.ws + P.dv_off) + wrow;
+  float mul_k, rs_k, mul_v, rs_v;
+  row_scale(amax_k * a.scale, a.scale, mul_k, rs_k);
+  row_scale(amax_v, 1.0f, mul_v, rs_v);
+  const int64_t wrow = (int64_t)it.unit * P.lmax + tk_row;
+  _Float16* krow_out = reinterpret_cast<_Float16*>(a.ws + P.dk_off) + wrow * D;
+  _Float16* vrow_out = reinterpret_cast<_Float16*>(a.ws + P.dv_off) + wrow * D;
 #pragma unroll
   for (int db = 0; db < DB; ++db)
 #pragma unroll
     for (int jj = 0; jj < 4; ++jj) {
       const int d = c0 + db * 32 + 8 * jj + 4 * hi;
-      *reinterpret_cast<f32x4*>(krow_out + d) =
-          f32x4{acc_dk[db][4 * jj] * a.scale, acc_dk[db][4 * jj + 1] * a.scale, acc_dk[db][4 * jj + 2] * a.scale,
-                acc_dk[db][4 * jj + 3] * a.scale};
-      *reinterpret_cast<f32x4*>(vrow_out + d) =
-          f32x4{acc_dv[db][4 * jj], acc_dv[db][4 * jj + 1], acc_dv[db][4 * jj + 2], acc_dv[db][4 * jj + 3]};
+      *reinterpret_cast<f16x4*>(krow_out + d) =
+          f16x4{(_Float16)(acc_dk[db][4 * jj] * mul_k), (_Float16)(acc_dk[db][4 * jj + 1] * mul_k),
+                (_Float16)(acc_dk[db][4 * jj + 2] * mul_k), (_Float16)(acc_dk[db][4 * jj + 3] * mul_k)};
+      *reinterpret_cast<f16x4*>(vrow_out + d) =
+          f16x4{(_Float16)(acc_dv[db][4 * jj] * mul_v), (_Float16)(acc_dv[db][4 * jj + 1] * mul_v),
+                (_Float16)(acc_dv[db][4 * jj + 2] * mul_v), (_Float16)(acc_dv[db][4 * jj + 3] * mul_v)};
     }
+  if (hi == 0) {
+    reinterpret_cast<float*>(a.ws + P.dk_rec_off)[wrow * kChunks<D> + half] = rs_k;
+    reinterpret_cast<float*>(a.ws + P.dv_rec_off)[wrow * kChunks<D> + half] = rs_v;
+  }
 }
 
 // ---------------------------------------------------------------------------
@@ -517,6 +556,7 @@ struct SumPat {
   FastDiv fw, fr;
   int32_t nseg, lmax;
   int64_t dq_off, dk_off, dv_off;
+  int64_t dq_rec_off, dk_rec_off, dv_rec_off;
 };
 
 struct SumArgs {
@@ -535,10 +575,15 @@ __device__ inline void store_bf16x8(u16* p, const f32x8& v) {
   __builtin_nontemporal_store(b, reinterpret_cast<bf16x8*>(p));
 }
 
-__device__ inline f32x8 load_f32x8(const float* p) {
-  const f32x4 x = __builtin_nontemporal_load(reinterpret_cast<const f32x4*>(p));
-  const f32x4 y = __builtin_nontemporal_load(reinterpret_cast<const f32x4*>(p + 4));
-  return f32x8{x[0], x[1], x[2], x[3], y[0], y[1], y[2], y[3]};
+// Eight elements of a compact gradient row, times the row chunk's scale.
+__device__ inline f32x8 load_scaled(const char* ws, int64_t off, int64_t rec_off, int64_t row, int64_t rec,
+                                    int d0) {
+  const f16x8 h = *reinterpret_cast<const f16x8*>(reinterpret_cast<const _Float16*>(ws + off) + row + d0);
+  const float sc = reinterpret_cast<const float*>(ws + rec_off)[rec];
+  f32x8 r;
+#pragma unroll
+  for (int e = 0; e < 8; ++e) r[e] = static_cast<float>(h[e]) * sc;
+  return r;
 }
 
 template <int D>
@@ -560,10 +605,11 @@ __global__ __launch_bounds__(kThreadsB) void bwd_sum(SumArgs a) {
     const uint32_t t = P.fr.div(pos);
     const uint32_t s = static_cast<uint32_t>(h) - P.fr.div(static_cast<uint32_t>(h)) * P.fr.d;
     if (pos - t * P.fr.d != s) continue;
-    const int64_t row = (((int64_t)bh * P.nseg + g) * P.lmax + t) * D + d0;
-    sq += load_f32x8(reinterpret_cast<const float*>(a.ws + P.dq_off) + row);
-    sk += load_f32x8(reinterpret_cast<const float*>(a.ws + P.dk_off) + row);
-    sv += load_f32x8(reinterpret_cast<const float*>(a.ws + P.dv_off) + row);
+    const int64_t crow = ((int64_t)bh * P.nseg + g) * P.lmax + t;
+    const int64_t rec = crow * kChunks<D> + (d0 / kCols<D>);
+    sq += load_scaled(a.ws, P.dq_off, P.dq_rec_off, crow * D, rec, d0);
+    sk += load_scaled(a.ws, P.dk_off, P.dk_rec_off, crow * D, rec, d0);
+    sv += load_scaled(a.ws, P.dv_off, P.dv_rec_off, crow * D, rec, d0);
   }
   const int64_t o = (((int64_t)b * a.N + p) * a.H + h) * D + d0;
   store_bf16x8(a.dq + o, sq);
@@ -630,14 +676,16 @@ hipError_t launch_backward(const Plan& plan, const BwdLayout& lay, const void* q
       bp = BwdPat{static_cast<int32_t>(pp.w), static_cast<int32_t>(pp.r), static_cast<int32_t>(pp.nseg),
                   static_cast<int32_t>(pp.lmax), static_cast<int32_t>(pp.ntiles), static_cast<int32_t>(pp.units),
                   static_cast<int64_t>(lay.dq_off[j]), static_cast<int64_t>(lay.dk_off[j]),
-                  static_cast<int64_t>(lay.dv_off[j])};
+                  static_cast<int64_t>(lay.dv_off[j]), static_cast<int64_t>(lay.dq_rec_off[j]),
+                  static_cast<int64_t>(lay.dk_rec_off[j]), static_cast<int64_t>(lay.dv_rec_off[j])};
       sp = SumPat{make_fastdiv(static_cast<uint32_t>(pp.w)), make_fastdiv(static_cast<uint32_t>(pp.r)),
                   static_cast<int32_t>(pp.nseg), static_cast<int32_t>(pp.lmax),
                   static_cast<int64_t>(lay.dq_off[j]), static_cast<int64_t>(lay.dk_off[j]),
-                  static_cast<int64_t>(lay.dv_off[j])};
+                  static_cast<int64_t>(lay.dv_off[j]), static_cast<int64_t>(lay.dq_rec_off[j]),
+                  static_cast<int64_t>(lay.dk_rec_off[j]), static_cast<int64_t>(lay.dv_rec_off[j])};
     } else {
-      bp = BwdPat{1, 1, 1, 1, 1, 0, 0, 0, 0};
-      sp = SumPat{make_fastdiv(1), make_fastdiv(1), 1, 1, 0, 0, 0};
+      bp = BwdPat{1, 1, 1, 1, 1, 0, 0, 0, 0, 0, 0, 0};
+      sp = SumPat{make_fastdiv(1), make_fastdiv(1), 1, 1, 0, 0, 0, 0, 0, 0};
     }
   }
   const dim3 rgrid(static_cast<unsigned>(rblocks));

@@ -69,22 +69,6 @@ struct SmemBf16 {
   int redo;  // set by a wave whose tile sums left the fast path's range
 };
 
-// The per-pattern output rows are stored as fp16 scaled by a power of two
-// per row: row t of a work item holds O_t * 2^-e_t with e_t chosen so that
-// the row's largest magnitude lands in [2^14, 2^15), and its record holds
-// (lse_t, 2^e_t).  The rows keep fp16's eleven significant bits relative to
-// the row's largest element and bf16's exponent range (Eq. 6 puts no bound
-// on the magnitude of a row).
-__device__ inline void row_scale(float amax_times_inv, float inv, float& mul, float& stored) {
-  // biased exponent E of the normalised row max a: a in [2^(E-127), 2^(E-126));
-  // a * 2^(141-E) is in [2^14, 2^15).  E is clamped to [15, 254] so that both
-  // powers of two are normal floats (rows below 2^-111 keep fewer bits).
-  int E = static_cast<int>((__builtin_bit_cast(unsigned, amax_times_inv) >> 23) & 0xff);
-  E = min(max(E, 15), 254);
-  mul = inv * __builtin_bit_cast(float, static_cast<unsigned>(268 - E) << 23);     // inv * 2^(141-E)
-  stored = __builtin_bit_cast(float, static_cast<unsigned>(E - 14) << 23);         // 2^(E-141)
-}
-
 template <int D, bool kBufferLoads>
 __global__ __launch_bounds__(kThreads) void attn_fwd_bf16(AttnArgs a) {
   static_assert(D % 32 == 0, "head dim must be a multiple of 32");

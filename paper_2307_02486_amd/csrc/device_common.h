@@ -216,6 +216,24 @@ __device__ inline void static_for(F&& f) {
   }
 }
 
+// Rows stored as fp16 scaled by a power of two per row (the forward pass's
+// per-pattern outputs, the backward pass's per-pattern gradients): a row x is
+// stored as x * 2^-e with e chosen so that the row's largest magnitude lands
+// in [2^14, 2^15), and 2^e is kept beside it.  The row keeps fp16's eleven
+// significant bits relative to its largest element and bf16's exponent range.
+// amax_times_inv = (largest |element| of the row) * inv, where inv is a factor
+// the row is multiplied by before it is stored; returns mul = inv * 2^-e (the
+// factor to apply) and stored = 2^e.
+__device__ inline void row_scale(float amax_times_inv, float inv, float& mul, float& stored) {
+  // biased exponent E of a = amax_times_inv: a in [2^(E-127), 2^(E-126));
+  // a * 2^(141-E) is in [2^14, 2^15).  E is clamped to [15, 254] so that both
+  // powers of two are normal floats (rows below 2^-111 keep fewer bits).
+  int E = static_cast<int>((__builtin_bit_cast(unsigned, amax_times_inv) >> 23) & 0xff);
+  E = min(max(E, 15), 254);
+  mul = inv * __builtin_bit_cast(float, static_cast<unsigned>(268 - E) << 23);     // inv * 2^(141-E)
+  stored = __builtin_bit_cast(float, static_cast<unsigned>(E - 14) << 23);         // 2^(E-141)
+}
+
 // Word 3 of a raw buffer resource on gfx9-family GPUs (32-bit data format,
 // no swizzle); with stride 0 the size field is a byte count and reads at or
 // beyond it return zero.

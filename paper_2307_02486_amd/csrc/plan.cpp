@@ -144,26 +144,35 @@ int make_bwd_layout(const Plan& p, BwdLayout* out) {
   ws = align_up(ws + rows_all * 4);
   l.nd_off = ws;
   ws = align_up(ws + rows_all * 4);
+  const uint64_t chunks = static_cast<uint64_t>(grad_chunks(p.D));
   for (int i = 0; i < p.npat; ++i) {
     const uint64_t rows = static_cast<uint64_t>(p.pat[i].units) * static_cast<uint64_t>(p.pat[i].lmax);
-    const uint64_t bytes = rows * static_cast<uint64_t>(p.D) * 4;
+    const uint64_t bytes = rows * static_cast<uint64_t>(p.D) * 2;  // fp16 rows
+    const uint64_t rec = rows * chunks * 4;                           // float scales
     l.dq_off[i] = ws;
     ws = align_up(ws + bytes);
     l.dk_off[i] = ws;
     ws = align_up(ws + bytes);
     l.dv_off[i] = ws;
     ws = align_up(ws + bytes);
+    l.dq_rec_off[i] = ws;
+    ws = align_up(ws + rec);
+    l.dk_rec_off[i] = ws;
+    ws = align_up(ws + rec);
+    l.dv_rec_off[i] = ws;
+    ws = align_up(ws + rec);
   }
   l.workspace_bytes = ws;
   const double D = static_cast<double>(p.D), es = 2.0, cov = static_cast<double>(p.covered_rows);
+  const double grad_row = D * 2.0 + 4.0 * static_cast<double>(chunks);  // a compact row and its scales
   l.flops = 2.5 * p.sparse_flops;
   // each gradient kernel reads the kept q, k, v, dout rows once and the two
-  // per-row scalars; dq writes one float32 row, dk/dv two
-  l.bytes_grad = cov * (2.0 * (4.0 * D * es + 8.0) + 3.0 * D * 4.0);
+  // per-row scalars; dq writes one compact row, dk/dv two
+  l.bytes_grad = cov * (2.0 * (4.0 * D * es + 8.0) + 3.0 * grad_row);
   // delta: out, dout and lse of every row read, two scalars written; sum:
   // the compact gradients read, dq, dk, dv written
   l.bytes_combine = static_cast<double>(rows_all) * (2.0 * D * es + 4.0 + 8.0 + 3.0 * D * es) +
-                    cov * 3.0 * D * 4.0;
+                    cov * 3.0 * grad_row;
   *out = l;
   return DA_OK;
 }

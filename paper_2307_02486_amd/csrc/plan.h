@@ -72,14 +72,25 @@ struct Plan {
 struct BwdLayout {
   uint64_t nl2_off;   // byte offset of -lse*log2(e)
   uint64_t nd_off;    // byte offset of -delta
+  // Per pattern, the compact gradients dq, dk, dv: fp16 rows [units*lmax][D],
+  // each row scaled by a power of two per chunk of kGradChunk columns, and
+  // the float scales [units*lmax][chunks] (see grad_chunks).
   uint64_t dq_off[DA_MAX_PATTERNS];
   uint64_t dk_off[DA_MAX_PATTERNS];
   uint64_t dv_off[DA_MAX_PATTERNS];
+  uint64_t dq_rec_off[DA_MAX_PATTERNS];
+  uint64_t dk_rec_off[DA_MAX_PATTERNS];
+  uint64_t dv_rec_off[DA_MAX_PATTERNS];
   uint64_t workspace_bytes;
   double flops;          // 10*D per unmasked pair
   double bytes_grad;     // algorithmic HBM bytes of the dq and dk/dv kernels
   double bytes_combine;  // algorithmic HBM bytes of the delta and sum kernels
 };
+
+// Columns of a compact gradient row that share one scale: the columns one
+// backward work item accumulates.
+constexpr int64_t kGradChunk = 64;
+inline int64_t grad_chunks(int64_t D) { return (D + kGradChunk - 1) / kGradChunk; }
 
 // Backward workspace and work of a validated forward plan.  DA_EUNSUPPORTED
 // unless the plan is bf16 (and for tiles whose offsets need 64 bits).

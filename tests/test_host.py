@@ -190,11 +190,13 @@ def test_profile_window_arguments(lib):
 
 def test_bwd_plan_accounting():
     """Backward workspace = two [B,H,N] float32 arrays plus, per pattern, three
-    float32 [units][lmax][D] blocks, each 256-byte aligned; flops = 10 D per pair."""
+    fp16 [units][lmax][D] blocks and three float32 [units][lmax][ceil(D/64)]
+    scale blocks, each 256-byte aligned; flops = 10 D per pair."""
     from paper_2307_02486_amd import plan, plan_bwd
     import torch
     for (B, N, H, D, pats) in [(1, 32768, 12, 64, [(2048, 1), (4096, 2), (8192, 4), (16384, 6), (32768, 12)]),
-                               (2, 777, 5, 32, [(256, 1), (512, 7), (1000, 9)])]:
+                               (2, 777, 5, 32, [(256, 1), (512, 7), (1000, 9)]),
+                               (1, 513, 17, 128, [(512, 1), (513, 20)])]:
         f = plan(B, N, H, D, pats, True, torch.bfloat16)
         b = plan_bwd(B, N, H, D, pats, True, torch.bfloat16)
         al = lambda x: (x + 255) // 256 * 256
@@ -203,7 +205,9 @@ def test_bwd_plan_accounting():
             w = min(w, N)
             rows = B * H * (-(-N // w)) * (-(-w // r))
             for _ in range(3):
-                ws = al(ws + rows * D * 4)
+                ws = al(ws + rows * D * 2)
+            for _ in range(3):
+                ws = al(ws + rows * (-(-D // 64)) * 4)
         assert b["workspace_bytes"] == ws
         assert b["sparse_flops"] == pytest.approx(2.5 * f["sparse_flops"], rel=1e-12)
         assert b["covered_rows"] == f["covered_rows"]
