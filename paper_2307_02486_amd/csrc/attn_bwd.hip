@@ -157,12 +157,16 @@ __global__ __launch_bounds__(kThreadsB) void bwd_delta(DeltaArgs a) {
   constexpr int RPB = kThreadsB / LPR; // rows per workgroup
   const int tid = __builtin_amdgcn_workitem_id_x();
   const int blk = __builtin_amdgcn_workgroup_id_x();
-  const int bh = blk / a.chunks;
-  const int p = (blk - bh * a.chunks) * RPB + tid / LPR;
+  // heads innermost, as in bwd_sum: the out and dout rows read together are adjacent
+  const int h = blk % a.H;
+  const int rest = blk / a.H;
+  const int chunk = rest % a.chunks;
+  const int b = rest / a.chunks;
+  const int bh = b * a.H + h;
+  const int p = chunk * RPB + tid / LPR;
   const int d0 = (tid % LPR) * 8;
   const bool ok = p < a.N;
   const int pp = ok ? p : a.N - 1;
-  const int h = bh % a.H, b = bh / a.H;
   const int64_t off = (((int64_t)b * a.N + pp) * a.H + h) * D + d0;
   const u32x4 o = __builtin_nontemporal_load(reinterpret_cast<const u32x4*>(a.out + off));
   const u32x4 g = __builtin_nontemporal_load(reinterpret_cast<const u32x4*>(a.dout + off));
@@ -592,11 +596,16 @@ __global__ __launch_bounds__(kThreadsB) void bwd_sum(SumArgs a) {
   constexpr int RPB = kThreadsB / LPR;
   const int tid = __builtin_amdgcn_workitem_id_x();
   const int blk = __builtin_amdgcn_workgroup_id_x();
-  const int bh = blk / a.chunks;
-  const int p = (blk - bh * a.chunks) * RPB + tid / LPR;
+  // heads innermost (launch index = (b * chunks + chunk) * H + h), as in the
+  // forward combine: workgroups running together write whole [H][D] spans
+  const int h = blk % a.H;
+  const int rest = blk / a.H;
+  const int chunk = rest % a.chunks;
+  const int b = rest / a.chunks;
+  const int bh = b * a.H + h;
+  const int p = chunk * RPB + tid / LPR;
   const int d0 = (tid % LPR) * 8;
   if (p >= a.N) return;
-  const int h = bh % a.H, b = bh / a.H;
   f32x8 sq = f32x8{0, 0, 0, 0, 0, 0, 0, 0}, sk = sq, sv = sq;
   for (int i = 0; i < a.npat; ++i) {
     const SumPat& P = a.pat[i];

@@ -9,6 +9,10 @@
 // lane owns eight consecutive head-dim elements of one row, so a row of a
 // per-pattern output is read with D/8 16-byte (fp16) or 32-byte (fp32) loads
 // and consecutive positions of a dense pattern are consecutive in memory.
+// Workgroups are launched with the head innermost, so that those running at
+// the same time write whole [H][D] spans of out (a position's rows of all
+// heads are adjacent): 3-9 % faster than one head's positions at a time,
+// whose row writes are H*D elements apart and land in as many DRAM pages.
 // A per-pattern row is stored divided by a power of two (its record's
 // scale), which multiplies the row's weight.
 // Whether pattern i keeps row p for head h, and at which compact index t,
@@ -37,7 +41,7 @@ struct CombArgs {
   void* out;
   float* lse;
   int32_t N, H, npat;
-  int32_t chunks;  // workgroups per (b, h)
+  int32_t chunks;  // workgroups per (b, h); launch index = (b * chunks + chunk) * H + h
   MixPat pat[DA_MAX_PATTERNS];
 };
 
@@ -89,11 +93,13 @@ __global__ __launch_bounds__(kThreads) void combine_fwd(CombArgs a) {
   constexpr int RPB = kThreads / LPR;   // rows per workgroup and pass
   const int tid = __builtin_amdgcn_workitem_id_x();
   const int blk = __builtin_amdgcn_workgroup_id_x();
-  const int bh = blk / a.chunks;
-  const int p0 = (blk - bh * a.chunks) * (RPB * kRows) + tid / LPR;
+  const int h = blk % a.H;
+  const int rest = blk / a.H;
+  const int chunk = rest % a.chunks;
+  const int b = rest / a.chunks;
+  const int bh = b * a.H + h;
+  const int p0 = chunk * (RPB * kRows) + tid / LPR;
   const int d0 = (tid % LPR) * 8;
-  const int h = bh % a.H;
-  const int b = bh / a.H;
 
   // Issue the loads of every pattern that keeps each of this lane's rows.
   typename Vec8<WsT>::type o[kRows][NP];
