@@ -16,7 +16,7 @@ pass times each step on its own (median, minimum, mean), once as is and once
 with a 512 MiB buffer written before each step so that the inputs are no
 longer held in the Infinity Cache.  Then the same call is timed on the
 N=262144 (H=16, D=64, 8 patterns) and N=1048576 (H=16, D=128, 6 patterns)
-workloads, whose per-pattern workspaces (2.2 and 8.7 GB) are far larger than
+workloads, whose per-pattern workspaces (1.1 and 8.7 GB) are far larger than
 the 256 MB Infinity Cache: their combine launch gives the combine's HBM rate.
 """
 from __future__ import annotations
@@ -63,6 +63,10 @@ def parse():
                     help="time the LongNet attention layer (LayerNorm, projections, xPos, dilated attention, "
                          "sub-LayerNorm, output projection) forward and forward+backward on the workload's "
                          "shape instead")
+    ap.add_argument("--per-pattern", action="store_true",
+                    help="instead of the benchmark: each pattern of the workload run alone (a one-pattern "
+                         "forward call), its attention launch timed against the MFMA peak; one JSON line "
+                         "per pattern (under a profiler each pattern's launches are separate dispatches)")
     ap.add_argument("--copy-calibration-mib", type=int, default=0,
                     help="only run a plain device-to-device copy of this many MiB (5 times), to "
                          "calibrate the HBM byte counters of a profiler against a known size")
@@ -398,6 +402,9 @@ def main():
     if args.layer:
         layer(args)
         return
+    if args.per_pattern:
+        per_pattern(args)
+        return
     import torch
 
     import workloads
@@ -516,6 +523,49 @@ def main():
         torch.cuda.empty_cache()
         res["large_workloads"] = [large_workload(workloads.BY_NAME[n], args) for n in names]
     print(json.dumps(res), flush=True)
+
+
+def per_pattern(args):
+    """Each (w, r) of the workload as a one-pattern problem: the attention
+    launch's mean duration over back-to-back calls after the warm-up, its
+    sparse FLOPs and the fraction of the MFMA peak.  The patterns run in the
+    workload's order, `steps` timed calls each."""
+    import torch
+
+    import workloads
+    from paper_2307_02486_amd import StageTimer, dilated_attn, plan, workspace_for
+    wl = workloads.BY_NAME[args.workload]
+    dev = torch.device("cuda:0")
+    stream = torch.cuda.current_stream(dev)
+    q, k, v = workloads.make_qkv(wl, device=dev)
+    out = torch.empty_like(q)
+    lse = torch.empty((wl.B, wl.H, wl.N), dtype=torch.float32, device=dev)
+    peak = PEAK_BF16_TFLOPS if wl.dtype == "bf16" else PEAK_F32_TFLOPS
+    for (w, r) in wl.patterns:
+        pats = [(w, r)]
+        info = plan(wl.B, wl.N, wl.H, wl.D, pats, wl.causal, wl.torch_dtype)
+        ws = workspace_for(q, pats, wl.causal)
+
+        def step():
+            dilated_attn(q, k, v, pats, wl.causal, out=out, lse=lse, workspace=ws, stream=stream)
+
+        t0, n = time.perf_counter(), 0
+        while n < args.warmup or time.perf_counter() - t0 < args.warmup_seconds:
+            step()
+            n += 1
+            torch.cuda.synchronize()
+        with StageTimer(capacity=args.steps) as st:
+            for _ in range(args.steps):
+                step()
+            torch.cuda.synchronize()
+        ms_attn = st.ms_attention / st.calls
+        tf = info["sparse_flops"] / (ms_attn * 1e-3) / 1e12
+        print(json.dumps({"workload": wl.name, "pattern": [w, r], "work_items": info["num_work_items"],
+                          "sparse_flops": info["sparse_flops"], "attention_ms": round(ms_attn, 5),
+                          "tflops": round(tf, 3), "frac_of_mfma_peak": round(tf / peak, 4),
+                          "calls": st.calls}), flush=True)
+        del ws
+        torch.cuda.empty_cache()
 
 
 def large_workload(wl, args):
