@@ -182,3 +182,29 @@ def test_backward_large_scores(scale_kind):
             gg, rr = gg[:, :, hs], rr[:, :, hs]
         e = _check(n, gg, rr, f"large scores {scale_kind}")
         note(f"[bwd] large scores {scale_kind} {n} err {e:.2e}")
+
+
+@pytest.mark.parametrize("gmax", [1e5, 1e-8])
+@pytest.mark.parametrize("shape,pats", [((1, 777, 3, 64), [(256, 1), (512, 7), (777, 3)]),
+                                        ((1, 513, 2, 128), [(512, 1), (513, 20)])],
+                         ids=["D64", "D128"])
+def test_backward_value_range(gmax, shape, pats):
+    """dout scaled so that the gradients reach about `gmax`: the per-pattern
+    gradients are stored as fp16 rows scaled by a power of two per 64-column
+    chunk, so neither 1e5 (above fp16's 65504) nor 1e-8 (below fp16's
+    smallest subnormal, 6e-8) loses relative precision.  Bar: 2e-2 of each tensor's largest magnitude
+    (the gradient bar, taken relative at every scale)."""
+    note(f"[bwd] value range {gmax:g} {shape} {pats}")
+    q = workloads.make_random(shape, torch.bfloat16, 1.0, 4545, "cuda", 0)
+    k = workloads.make_random(shape, torch.bfloat16, 1.0, 4545, "cuda", 1)
+    v = workloads.make_random(shape, torch.bfloat16, 1.0, 4545, "cuda", 2)
+    dout = (workloads.make_random(shape, torch.float32, 1.0, 4545, "cuda", 3) * gmax).to(torch.bfloat16)
+    dq, dk, dv = _gpu_bwd(q, k, v, dout, pats, True)
+    rq, rk, rv, _, _ = oracle.dilated_attention_bwd_ref(to64(q), to64(k), to64(v), to64(dout), pats, True)
+    for n, g, r in (("dq", dq, rq), ("dk", dk, rk), ("dv", dv, rv)):
+        got = to64(g)
+        assert np.isfinite(got).all(), f"{n}: not finite"
+        top = float(np.abs(r).max())
+        err = float(np.abs(got - r).max())
+        assert err <= REL * top, f"{n}: max-abs err {err:.3e} > {REL * top:.3e} (max |ref| {top:.3e})"
+        note(f"[bwd] value range {gmax:g} {shape}: {n} err/max {err / top:.2e}")
