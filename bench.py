@@ -36,6 +36,8 @@ PEAK_BF16_TFLOPS = 2500.0     # MI355X dense bf16 MFMA
 PEAK_F32_TFLOPS = 157.3       # MI355X fp32 vector
 PEAK_HBM_GBS = 8000.0         # MI355X HBM3E
 PROFILED_TRAFFIC = os.path.join(ROOT, "profiles", "traffic.json")
+# Sources of the two forward kernels whose hashes key the profiled figures.
+PROFILED_SOURCES = ("attn_fwd.hip", "combine.hip", "device_common.h", "kernels.h")
 
 
 def parse():
@@ -105,8 +107,8 @@ def profiled_counters(workload):
     """Per-launch figures measured with rocprofv3 counters for the current
     kernel sources: HBM bytes of the attention and combine kernels
     (FETCH_SIZE / WRITE_SIZE scaled by a plain copy of known size) and the
-    attention kernel's MFMA busy percentage.  Empty when the attention or the
-    combine kernel's source changed since the measurement."""
+    attention kernel's MFMA busy percentage.  Empty when a source of the
+    attention or the combine kernel changed since the measurement."""
     import hashlib
     if not os.path.exists(PROFILED_TRAFFIC):
         return {}
@@ -114,11 +116,10 @@ def profiled_counters(workload):
         rec = json.load(f).get(workload)
     if not rec:
         return {}
-    for name in ("attn_fwd", "combine"):
-        src = os.path.join(ROOT, "paper_2307_02486_amd", "csrc", name + ".hip")
-        with open(src, "rb") as f:
+    for name in PROFILED_SOURCES:
+        with open(os.path.join(ROOT, "paper_2307_02486_amd", "csrc", name), "rb") as f:
             sha = hashlib.sha256(f.read()).hexdigest()[:16]
-        if sha != rec.get(name + "_hip_sha256_16"):
+        if sha != rec.get(name.replace(".", "_") + "_sha256_16"):
             return {}
     return rec
 

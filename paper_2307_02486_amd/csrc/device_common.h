@@ -48,8 +48,9 @@ struct Item {
 // so launch index x is mapped to XCD c = x mod 8 and the units with index = c
 // (mod 8) are given to that XCD: the query tiles of one segment run on one
 // XCD and its K/V rows are fetched into that XCD's L2 once.  (A pattern whose
-// unit count is not a multiple of 8 has its long query tiles dealt to the
-// XCDs one by one instead, trading L2 reuse for balance.)  On each XCD the
+// unit count is not a multiple of 8 has the long query tiles of its last
+// units mod 8 units dealt to the XCDs one by one instead, trading their L2
+// reuse for balance.)  On each XCD the
 // items come in two phases.  First, pattern by pattern (in the order of the
 // records, those with the most query tiles per segment first) and unit by unit, the query tiles from the
 // last (the longest under a causal mask) down to tile kShortTiles, so the
@@ -89,18 +90,30 @@ __device__ inline bool decode_item(const Args& a, int bid, int block_m, Item& it
       slot -= n;
     } else {
       // A unit count that is not a multiple of 8 would load the XCDs
-      // unevenly: the pattern's long items f = unit * nlong + (ntiles-1-tq)
-      // are dealt to the XCDs one by one instead (f = c mod 8 to XCD c).
-      const int total = P.units * nlong;
-      const int n = total > c ? (total - c + 7) >> 3 : 0;
-      if (slot < n) {
+      // unevenly: the first units8 = units - units mod 8 units go to the
+      // XCDs whole as above, and the long items f = (unit - units8) * nlong +
+      // (ntiles-1-tq) of the remaining ones are dealt to the XCDs one by one
+      // (f = c mod 8 to XCD c), trading their L2 reuse for balance.
+      const int units8 = P.units & ~7;
+      const int na = (units8 >> 3) * nlong;
+      if (slot < na) {
         pi = p;
-        const int f = c + 8 * slot;
-        unit = f / nlong;
-        tq = P.ntiles - 1 - (f - unit * nlong);
+        const int j = slot / nlong;
+        unit = c + 8 * j;
+        tq = P.ntiles - 1 - (slot - j * nlong);
         break;
       }
-      slot -= n;
+      const int rest = (P.units - units8) * nlong;
+      const int nb = rest > c ? (rest - c + 7) >> 3 : 0;
+      if (slot - na < nb) {
+        pi = p;
+        const int f = c + 8 * (slot - na);
+        const int j = f / nlong;
+        unit = units8 + j;
+        tq = P.ntiles - 1 - (f - j * nlong);
+        break;
+      }
+      slot -= na + nb;
     }
   }
 #pragma unroll

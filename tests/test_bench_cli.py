@@ -19,20 +19,21 @@ def test_more_than_one_gpu_is_refused_with_a_message():
 
 
 def _sha(name):
-    with open(os.path.join(ROOT, "paper_2307_02486_amd", "csrc", name + ".hip"), "rb") as f:
+    with open(os.path.join(ROOT, "paper_2307_02486_amd", "csrc", name), "rb") as f:
         return hashlib.sha256(f.read()).hexdigest()[:16]
 
 
 def test_profiled_counters_follow_the_kernel_sources(tmp_path, monkeypatch):
-    rec = {"attention_bytes_per_launch": 123, "combine_bytes_per_launch": 45,
-           "attention_mfma_busy_pct": 40.0, "attn_fwd_hip_sha256_16": _sha("attn_fwd"),
-           "combine_hip_sha256_16": _sha("combine")}
+    keys = [n.replace(".", "_") + "_sha256_16" for n in bench.PROFILED_SOURCES]
+    assert "device_common_h_sha256_16" in keys   # the shared header changes both kernels
+    rec = {"attention_bytes_per_launch": 123, "combine_bytes_per_launch": 45, "attention_mfma_busy_pct": 40.0}
+    rec.update({k: _sha(n) for k, n in zip(keys, bench.PROFILED_SOURCES)})
     path = tmp_path / "traffic.json"
     monkeypatch.setattr(bench, "PROFILED_TRAFFIC", str(path))
     assert bench.profiled_counters("w") == {}                 # no file
     path.write_text(json.dumps({"w": rec}))
     assert bench.profiled_counters("w") == rec                # sources unchanged
     assert bench.profiled_counters("other") == {}             # workload never profiled
-    for key in ("attn_fwd_hip_sha256_16", "combine_hip_sha256_16"):
+    for key in keys:
         path.write_text(json.dumps({"w": dict(rec, **{key: "0" * 16})}))
         assert bench.profiled_counters("w") == {}             # a kernel changed since: no figures
